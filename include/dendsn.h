@@ -1,0 +1,159 @@
+/*
+ * dendsn.h — C ABI of the DendSN layer scan on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes one layer of dendritic spiking neurons (DendSN) over T
+ * time steps and the surrogate-gradient backpropagation through time of the
+ * same layer, as defined in "Scalable Dendritic Modeling Advances Expressive
+ * and Robust Deep Spiking Neural Networks" (Huang et al., arXiv 2412.06355):
+ *
+ *   Methods, "Dendritic spiking neuron":
+ *     Eq. (methods-compartment)        Vd_b[t] = alpha Vd_b[t-1] + X_b[t],  Vd[0] = 0
+ *     Eq. (methods-branch-aggregation) Y_b[t]  = psi(|Vd_b[t] - xi_b| / zeta_b)   (one compartment per branch)
+ *     Eq. (methods-mexican-hat)        psi(x)  = (1 - x^2) exp(-x^2/2), or psi(x) = x
+ *     Eq. (methods-soma-input)         Z[t]    = sum_b kappa_b Y_b[t]
+ *     Eq. (methods-lif-reset-charge)   H[t]    = beta (1 - S[t-1]) H[t-1] + Z[t],  H[0] = S[0] = 0
+ *     Eq. (methods-lif-fire)           S[t]    = 1 if H[t] - v_th >= 0 else 0
+ *   Methods, "DendSN variants": Stateless Dendrite (Vd_b[t] = X_b[t]).
+ *   Methods, "Dendritic branch gating": kappa* = kappa (.) m with a fixed binary
+ *     mask m per task, Eq. (methods-dbg-mask) and Eq. (methods-dbg-sampling).
+ *   Methods, "Dendritic spiking neural networks": layer form — neurons of one
+ *     channel share xi, zeta, kappa; alpha is shared by the whole layer; the
+ *     backward replaces Theta' by a surrogate derivative, Eq. (methods-sg).
+ *
+ * Layout (all row-major):
+ *   X, grad_x          [T, N, B]  branches innermost, I/O dtype (fp32 or bf16)
+ *   spikes, grad_spikes[T, N]     I/O dtype; spikes are exactly 0.0 or 1.0
+ *   v_soma, grad_v_soma[T, N]     fp32; v_soma[t] = H[t], the potential before the reset
+ *   kappa, xi, zeta    [C, B]     fp32 per-channel parameters
+ *   mask               [C, B]     uint8, nonzero = branch kept
+ *   alpha              [1]        fp32 on the device (a learnable layer scalar)
+ *   Neuron n = (b_idx * C + c) * S + s for batch item b_idx, channel c, spatial
+ *   position s; a fully connected layer has S = 1.
+ *
+ * Conventions:
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
+ *     allocates nothing, keeps no state between calls and never synchronises:
+ *     both calls enqueue kernels on the given stream and return.
+ *   - X, grad_x, ckpt and workspace must be 16-byte aligned; every other tensor
+ *     must be aligned to its element size.
+ *   - Outputs are overwritten, never accumulated.
+ *   - Every argument check runs on the host before anything is launched.  On
+ *     failure the call returns a status, writes nothing, and a description of the
+ *     first failed check is available from dendsn_last_error() on the calling
+ *     thread.  A failed launch returns DENDSN_E_HIP.  Faults inside a kernel
+ *     surface at the caller's next synchronisation.
+ *   - Not checked (it would need a device synchronisation): zeta > 0,
+ *     0 <= alpha < 1, finite inputs, and that pointers address device memory of
+ *     the stated size.
+ */
+#ifndef DENDSN_H
+#define DENDSN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dendsn_status {
+    DENDSN_OK = 0,
+    DENDSN_E_INVALID = 1,      /* an argument violates the contract            */
+    DENDSN_E_UNSUPPORTED = 2,  /* valid model, but a shape this build rejects   */
+    DENDSN_E_WORKSPACE = 3,    /* workspace missing or smaller than required    */
+    DENDSN_E_HIP = 4           /* a kernel launch failed                        */
+} dendsn_status;
+
+typedef enum dendsn_io { DENDSN_IO_F32 = 0, DENDSN_IO_BF16 = 1 } dendsn_io;
+typedef enum dendsn_psi { DENDSN_PSI_IDENTITY = 0, DENDSN_PSI_MEXHAT = 1 } dendsn_psi;
+typedef enum dendsn_sg { DENDSN_SG_ATAN = 0, DENDSN_SG_SIGMOID = 1 } dendsn_sg;
+
+typedef struct dendsn_cfg {
+    int64_t T;                 /* time steps, >= 1                                         */
+    int64_t batch;             /* batch items, >= 1                                        */
+    int64_t C;                 /* channels (parameter sets), >= 1                          */
+    int64_t S;                 /* spatial positions per channel, >= 1 (1 = fully connected)*/
+    int32_t B;                 /* branches per neuron, 1..128                              */
+    int32_t comps_per_branch;  /* compartments per branch (P / B); must be 1               */
+    int32_t stateful;          /* 1: leaky compartments; 0: Stateless Dendrite             */
+    int32_t detach_reset;      /* 1: no gradient through the reset factor (1 - S[t-1])     */
+    int32_t ckpt_every;        /* K >= 1: state checkpoint after every K steps (K >= T: none) */
+    int32_t io;                /* dendsn_io: storage of X, spikes, grad_x, grad_spikes     */
+    int32_t psi;               /* dendsn_psi: dendritic activation                          */
+    int32_t sg;                /* dendsn_sg: surrogate derivative used by the backward      */
+    float sg_scale;            /* slope a of the sigmoid surrogate sigma(a x); > 0          */
+    float beta;                /* somatic decay, 0 <= beta < 1                              */
+    float v_th;                /* firing threshold (the paper uses 1)                       */
+    int32_t batch_groups;      /* tuning: batch groups per launch, 0 = automatic           */
+} dendsn_cfg;
+
+/*
+ * Size in bytes of the state-checkpoint buffer that dendsn_forward fills and
+ * dendsn_backward reads: nck * N * (B + 1) * 4 with nck = ceil(T / K) - 1
+ * (the dendritic state and the somatic potential after steps K, 2K, ... < T).
+ * Zero when K >= T.  Returns DENDSN_E_INVALID / _UNSUPPORTED for a bad cfg.
+ */
+dendsn_status dendsn_ckpt_bytes(const dendsn_cfg* cfg, size_t* bytes);
+
+/*
+ * Size in bytes of the scratch workspace dendsn_backward needs for its
+ * per-block parameter-gradient partials (always > 0).  It depends on the whole
+ * cfg, including batch_groups.
+ */
+dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes);
+
+/*
+ * Forward scan over t = 1..T (equations above).
+ *   x       [T,N,B] io    required
+ *   alpha   [1] fp32      required when cfg->stateful, ignored otherwise
+ *   kappa   [C,B] fp32    required
+ *   xi      [C,B] fp32    NULL means 0
+ *   zeta    [C,B] fp32    NULL means 1
+ *   mask    [C,B] uint8   NULL means every branch kept
+ *   spikes  [T,N] io      required output
+ *   v_soma  [T,N] fp32    optional output (NULL: not written)
+ *   ckpt    dendsn_ckpt_bytes bytes, optional output; NULL is allowed only for
+ *           inference (no backward will follow), or when K >= T.
+ */
+dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* alpha,
+                             const float* kappa, const float* xi, const float* zeta,
+                             const uint8_t* mask, void* spikes, float* v_soma, float* ckpt,
+                             hipStream_t stream);
+
+/*
+ * Backward scan: gradients of  sum(grad_spikes * S) + sum(grad_v_soma * H)  with
+ * Theta'(H - v_th) replaced by the surrogate cfg->sg, through time (BPTT).
+ * The dendrite is recomputed from x and the checkpoints (gradient
+ * checkpointing); nothing else of the forward is stored.  The call must use the
+ * same cfg, x, alpha, kappa, xi, zeta and mask as the forward that wrote ckpt.
+ *   ckpt         required when nck > 0 (see dendsn_ckpt_bytes)
+ *   grad_spikes  [T,N] io     required
+ *   grad_v_soma  [T,N] fp32   NULL means 0
+ *   grad_x       [T,N,B] io   required output
+ *   grad_alpha   [1] fp32     optional output (0 for the Stateless Dendrite)
+ *   grad_kappa, grad_xi, grad_zeta  [C,B] fp32 optional outputs, summed over
+ *                time, batch and spatial positions; exactly 0 where the mask is 0.
+ *   workspace    device scratch of at least dendsn_bwd_workspace_bytes bytes,
+ *                clobbered by the call.
+ * Results are deterministic: the same inputs give bit-identical outputs.
+ */
+dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha,
+                              const float* kappa, const float* xi, const float* zeta,
+                              const uint8_t* mask, const float* ckpt, const void* grad_spikes,
+                              const float* grad_v_soma, void* grad_x, float* grad_alpha,
+                              float* grad_kappa, float* grad_xi, float* grad_zeta,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Static name of a status code. */
+const char* dendsn_status_str(dendsn_status status);
+
+/* Description of the last failed check on the calling thread ("" if none). */
+const char* dendsn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DENDSN_H */

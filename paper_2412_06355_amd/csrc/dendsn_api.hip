@@ -1,0 +1,314 @@
+// C ABI of the DendSN layer scan: argument checks, launch planning, dispatch,
+// and the deterministic parameter-gradient finalize kernel.
+#include <math.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/dendsn.h"
+#include "dendsn_kernels.h"
+
+namespace dendsn {
+
+hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream);
+hipError_t launch_fwd_bf16(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream);
+hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+
+__global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
+  const int tid = threadIdx.x;
+  if (blockIdx.x == gridDim.x - 1) {
+    __shared__ double sh[kThreads];
+    double s = 0.0;
+    for (int64_t i = tid; i < f.nA; i += kThreads) s += double(f.wsA[i]);
+    sh[tid] = s;
+    __syncthreads();
+    for (int w = kThreads / 2; w >= 1; w >>= 1) {
+      if (tid < w) sh[tid] += sh[tid + w];
+      __syncthreads();
+    }
+    if (tid == 0 && f.ga) f.ga[0] = f.stateful ? float(sh[0]) : 0.0f;
+    return;
+  }
+  const int64_t o = int64_t(blockIdx.x) * kThreads + tid;
+  if (o >= f.C * f.B) return;
+  const int64_t c = o / f.B;
+  const int b = int(o % f.B);
+  const bool on = f.mask ? (f.mask[o] != 0) : true;
+  float* outs[3] = {f.gk, f.gxi, f.gz};
+  for (int q = 0; q < 3; ++q) {
+    if (!outs[q]) continue;
+    double s = 0.0;
+    for (int g = 0; g < f.G; ++g)
+      for (int j = 0; j < f.tpc; ++j)
+        s += double(f.wsP[((int64_t(g) * f.C + c) * f.tpc + j) * 3 * f.B + q * f.B + b]);
+    outs[q][o] = on ? float(s) : 0.0f;
+  }
+}
+
+}  // namespace dendsn
+
+using namespace dendsn;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dendsn_status fail(dendsn_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// (BL, L): a vector-width lane split when the branch count allows one, else a
+// generic split with up to 8 branches per lane over 1 or 2 lanes.
+bool choose_mapping(int B, int io, int* BL, int* L, int* fast) {
+  const int blv = (io == DENDSN_IO_BF16 && B % 8 == 0) ? 8 : 4;
+  if (B % blv == 0 && is_pow2(B / blv) && B / blv <= 16) {
+    *BL = blv; *L = B / blv; *fast = 1;
+    return true;
+  }
+  for (int l = 1; l <= 2; l *= 2) {
+    if (B % l == 0 && B / l <= 8) {
+      *BL = B / l; *L = l; *fast = 0;
+      return true;
+    }
+  }
+  return false;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+dendsn_status check_cfg(const dendsn_cfg* c) {
+  if (!c) return fail(DENDSN_E_INVALID, "cfg is NULL");
+  if (c->T < 1 || c->T > INT32_MAX) return fail(DENDSN_E_INVALID, "T must be in [1, 2^31)");
+  if (c->batch < 1) return fail(DENDSN_E_INVALID, "batch must be >= 1");
+  if (c->C < 1) return fail(DENDSN_E_INVALID, "C must be >= 1");
+  if (c->S < 1) return fail(DENDSN_E_INVALID, "S must be >= 1");
+  if (c->B < 1 || c->B > 128) return fail(DENDSN_E_INVALID, "B must be in [1, 128]");
+  if (c->comps_per_branch < 1) return fail(DENDSN_E_INVALID, "comps_per_branch must be >= 1");
+  if (c->comps_per_branch != 1)
+    return fail(DENDSN_E_UNSUPPORTED, "only one compartment per branch (P == B) is supported");
+  if (c->stateful != 0 && c->stateful != 1) return fail(DENDSN_E_INVALID, "stateful must be 0 or 1");
+  if (c->detach_reset != 0 && c->detach_reset != 1)
+    return fail(DENDSN_E_INVALID, "detach_reset must be 0 or 1");
+  if (c->ckpt_every < 1) return fail(DENDSN_E_INVALID, "ckpt_every must be >= 1");
+  if (c->io != DENDSN_IO_F32 && c->io != DENDSN_IO_BF16) return fail(DENDSN_E_INVALID, "bad io");
+  if (c->psi != DENDSN_PSI_IDENTITY && c->psi != DENDSN_PSI_MEXHAT) return fail(DENDSN_E_INVALID, "bad psi");
+  if (c->sg != DENDSN_SG_ATAN && c->sg != DENDSN_SG_SIGMOID) return fail(DENDSN_E_INVALID, "bad sg");
+  if (c->sg == DENDSN_SG_SIGMOID && !(isfinite(c->sg_scale) && c->sg_scale > 0.0f))
+    return fail(DENDSN_E_INVALID, "sg_scale must be finite and > 0");
+  if (!isfinite(c->beta)) return fail(DENDSN_E_INVALID, "beta must be finite");
+  if (!isfinite(c->v_th)) return fail(DENDSN_E_INVALID, "v_th must be finite");
+  if (c->batch_groups < 0) return fail(DENDSN_E_INVALID, "batch_groups must be >= 0");
+  // N and T * N * B must fit comfortably in int64 element counts.
+  const int64_t lim = int64_t(1) << 46;
+  if (c->batch > lim / c->C || c->batch * c->C > lim / c->S) return fail(DENDSN_E_INVALID, "N too large");
+  const int64_t N = c->batch * c->C * c->S;
+  if (N > (lim / c->B) / c->T) return fail(DENDSN_E_INVALID, "T * N * B too large");
+  int BL, L, fast;
+  if (!choose_mapping(c->B, c->io, &BL, &L, &fast))
+    return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build");
+  return DENDSN_OK;
+}
+
+// Tiling and batch grouping.  Same mapping and tiling rules in both directions,
+// so the backward's recompute adds the branch terms in the forward's order.
+Plan make_plan(const dendsn_cfg* c, bool bwd) {
+  Plan p;
+  memset(&p, 0, sizeof(p));
+  choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
+  const int L = p.L;
+  if (c->S >= kThreads / L) {
+    p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
+    p.tpc = int32_t(ceil_div(c->S, p.pb)); p.cpt = 1;
+    p.ntiles = c->C * p.tpc;
+  } else if (c->S == 1) {
+    p.mode = kFC; p.ways = 4; p.pb = 64 / L;
+    p.tpc = 1; p.cpt = p.pb;
+    p.ntiles = ceil_div(c->C, p.cpt);
+  } else {
+    p.mode = kSeg; p.ways = 1; p.pb = kThreads / L;
+    p.tpc = 1; p.cpt = int32_t(p.pb / c->S);
+    p.ntiles = ceil_div(c->C, p.cpt);
+  }
+  const int64_t target_waves = 16384;
+  int64_t G = ceil_div(target_waves, p.ntiles * 4);
+  G = G < 1 ? 1 : G;
+  const int64_t max_g = ceil_div(c->batch, p.ways);
+  if (G > max_g) G = max_g;
+  if (bwd && p.mode != kSpatial && G > 8) G = 8;  // bounds the per-group partials
+  if (c->batch_groups > 0) G = c->batch_groups < c->batch ? c->batch_groups : c->batch;
+  p.bpg = int32_t(ceil_div(c->batch, G));
+  p.G = int32_t(ceil_div(c->batch, p.bpg));
+  const int64_t Ke = c->ckpt_every < c->T ? c->ckpt_every : c->T;
+  p.nck = int32_t(ceil_div(c->T, c->ckpt_every) - 1);
+  p.KS = (p.fast && p.BL <= 4 && Ke >= 8) ? 8 : 4;
+  return p;
+}
+
+size_t ckpt_bytes(const dendsn_cfg* c, const Plan& p) {
+  const int64_t N = c->batch * c->C * c->S;
+  return size_t(p.nck) * size_t(N) * size_t(c->B + 1) * sizeof(float);
+}
+
+void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) {
+  const size_t nP = size_t(p.G) * size_t(c->C) * size_t(p.tpc) * 3 * size_t(c->B);
+  const size_t nA = size_t(p.G) * size_t(p.ntiles);
+  *offA = ((nP * sizeof(float) + 255) / 256) * 256;
+  *total = *offA + nA * sizeof(float);
+}
+
+dendsn_status check_grid(const Plan& p) {
+  if (p.ntiles * p.G > int64_t(INT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "grid too large");
+  return DENDSN_OK;
+}
+
+void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* alpha, const float* kappa,
+               const float* xi, const float* zeta, const uint8_t* mask, ScanArgs* s) {
+  s->x = x;
+  s->alpha = c->stateful ? alpha : nullptr;
+  s->kappa = kappa; s->xi = xi; s->zeta = zeta; s->mask = mask;
+  s->T = c->T; s->C = c->C; s->S = c->S; s->batch = c->batch;
+  s->M = c->C * c->S; s->N = c->batch * s->M;
+  s->B = c->B;
+  s->K = int32_t(c->ckpt_every < c->T ? c->ckpt_every : c->T);
+  s->nck = p.nck;
+  s->beta = c->beta; s->vth = c->v_th;
+  s->mode = p.mode; s->ways = p.ways; s->pb = p.pb; s->tpc = p.tpc; s->cpt = p.cpt;
+  s->bpg = p.bpg; s->ntiles = p.ntiles;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dendsn_status_str(dendsn_status st) {
+  switch (st) {
+    case DENDSN_OK: return "DENDSN_OK";
+    case DENDSN_E_INVALID: return "DENDSN_E_INVALID";
+    case DENDSN_E_UNSUPPORTED: return "DENDSN_E_UNSUPPORTED";
+    case DENDSN_E_WORKSPACE: return "DENDSN_E_WORKSPACE";
+    case DENDSN_E_HIP: return "DENDSN_E_HIP";
+  }
+  return "DENDSN_UNKNOWN_STATUS";
+}
+
+const char* dendsn_last_error(void) { return g_last_error.c_str(); }
+
+dendsn_status dendsn_ckpt_bytes(const dendsn_cfg* cfg, size_t* bytes) {
+  g_last_error.clear();
+  dendsn_status st = check_cfg(cfg);
+  if (st != DENDSN_OK) return st;
+  if (!bytes) return fail(DENDSN_E_INVALID, "bytes is NULL");
+  *bytes = ckpt_bytes(cfg, make_plan(cfg, false));
+  return DENDSN_OK;
+}
+
+dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes) {
+  g_last_error.clear();
+  dendsn_status st = check_cfg(cfg);
+  if (st != DENDSN_OK) return st;
+  if (!bytes) return fail(DENDSN_E_INVALID, "bytes is NULL");
+  size_t offA, total;
+  ws_layout(cfg, make_plan(cfg, true), &offA, &total);
+  *bytes = total;
+  return DENDSN_OK;
+}
+
+dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* kappa,
+                             const float* xi, const float* zeta, const uint8_t* mask, void* spikes,
+                             float* v_soma, float* ckpt, hipStream_t stream) {
+  g_last_error.clear();
+  dendsn_status st = check_cfg(cfg);
+  if (st != DENDSN_OK) return st;
+  if (!x) return fail(DENDSN_E_INVALID, "x is NULL");
+  if (!kappa) return fail(DENDSN_E_INVALID, "kappa is NULL");
+  if (!spikes) return fail(DENDSN_E_INVALID, "spikes is NULL");
+  if (cfg->stateful && !alpha) return fail(DENDSN_E_INVALID, "alpha is NULL for a stateful dendrite");
+  const size_t esz = cfg->io == DENDSN_IO_BF16 ? 2 : 4;
+  if (!aligned(x, 16)) return fail(DENDSN_E_INVALID, "x must be 16-byte aligned");
+  if (!aligned(spikes, esz)) return fail(DENDSN_E_INVALID, "spikes misaligned");
+  if (ckpt && !aligned(ckpt, 16)) return fail(DENDSN_E_INVALID, "ckpt must be 16-byte aligned");
+  if ((alpha && !aligned(alpha, 4)) || !aligned(kappa, 4) || (xi && !aligned(xi, 4)) ||
+      (zeta && !aligned(zeta, 4)) || (v_soma && !aligned(v_soma, 4)))
+    return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
+  const Plan p = make_plan(cfg, false);
+  if ((st = check_grid(p)) != DENDSN_OK) return st;
+  FwdArgs fa;
+  memset(&fa, 0, sizeof(fa));
+  fill_scan(cfg, p, x, alpha, kappa, xi, zeta, mask, &fa.s);
+  fa.spikes = spikes;
+  fa.vsoma = v_soma;
+  fa.ckpt = p.nck > 0 ? ckpt : nullptr;
+  const hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_fwd_bf16(p, fa, cfg->psi, stream)
+                                                 : launch_fwd_f32(p, fa, cfg->psi, stream);
+  if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("forward launch: ") + hipGetErrorString(e));
+  return DENDSN_OK;
+}
+
+dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* kappa,
+                              const float* xi, const float* zeta, const uint8_t* mask, const float* ckpt,
+                              const void* grad_spikes, const float* grad_v_soma, void* grad_x,
+                              float* grad_alpha, float* grad_kappa, float* grad_xi, float* grad_zeta,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_last_error.clear();
+  dendsn_status st = check_cfg(cfg);
+  if (st != DENDSN_OK) return st;
+  if (!x) return fail(DENDSN_E_INVALID, "x is NULL");
+  if (!kappa) return fail(DENDSN_E_INVALID, "kappa is NULL");
+  if (!grad_spikes) return fail(DENDSN_E_INVALID, "grad_spikes is NULL");
+  if (!grad_x) return fail(DENDSN_E_INVALID, "grad_x is NULL");
+  if (cfg->stateful && !alpha) return fail(DENDSN_E_INVALID, "alpha is NULL for a stateful dendrite");
+  const Plan p = make_plan(cfg, true);
+  if (p.nck > 0 && !ckpt) return fail(DENDSN_E_INVALID, "ckpt is NULL but the forward wrote checkpoints");
+  const size_t esz = cfg->io == DENDSN_IO_BF16 ? 2 : 4;
+  if (!aligned(x, 16) || !aligned(grad_x, 16)) return fail(DENDSN_E_INVALID, "x / grad_x must be 16-byte aligned");
+  if (ckpt && !aligned(ckpt, 16)) return fail(DENDSN_E_INVALID, "ckpt must be 16-byte aligned");
+  if (!aligned(grad_spikes, esz)) return fail(DENDSN_E_INVALID, "grad_spikes misaligned");
+  if ((alpha && !aligned(alpha, 4)) || !aligned(kappa, 4) || (xi && !aligned(xi, 4)) ||
+      (zeta && !aligned(zeta, 4)) || (grad_v_soma && !aligned(grad_v_soma, 4)) ||
+      (grad_alpha && !aligned(grad_alpha, 4)) || (grad_kappa && !aligned(grad_kappa, 4)) ||
+      (grad_xi && !aligned(grad_xi, 4)) || (grad_zeta && !aligned(grad_zeta, 4)))
+    return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
+  size_t offA, total;
+  ws_layout(cfg, p, &offA, &total);
+  if (!workspace) return fail(DENDSN_E_WORKSPACE, "workspace is NULL");
+  if (!aligned(workspace, 16)) return fail(DENDSN_E_WORKSPACE, "workspace must be 16-byte aligned");
+  if (workspace_bytes < total)
+    return fail(DENDSN_E_WORKSPACE, "workspace smaller than dendsn_bwd_workspace_bytes()");
+  if ((st = check_grid(p)) != DENDSN_OK) return st;
+
+  BwdArgs ba;
+  memset(&ba, 0, sizeof(ba));
+  fill_scan(cfg, p, x, alpha, kappa, xi, zeta, mask, &ba.s);
+  ba.ckpt = ckpt;
+  ba.gspk = grad_spikes;
+  ba.gv = grad_v_soma;
+  ba.gx = grad_x;
+  ba.wsP = static_cast<float*>(workspace);
+  ba.wsA = reinterpret_cast<float*>(static_cast<char*>(workspace) + offA);
+  ba.detach = cfg->detach_reset;
+  ba.sg = cfg->sg;
+  ba.sg_scale = cfg->sg_scale;
+  hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_bwd_bf16(p, ba, cfg->psi, stream)
+                                           : launch_bwd_f32(p, ba, cfg->psi, stream);
+  if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("backward launch: ") + hipGetErrorString(e));
+
+  FinArgs f;
+  memset(&f, 0, sizeof(f));
+  f.wsP = ba.wsP; f.wsA = ba.wsA; f.mask = mask;
+  f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha;
+  f.C = cfg->C; f.B = cfg->B; f.G = p.G; f.tpc = p.tpc; f.stateful = cfg->stateful;
+  f.nA = int64_t(p.G) * p.ntiles;
+  const int64_t nblk = ceil_div(cfg->C * cfg->B, kThreads) + 1;
+  dendsn_finalize_kernel<<<dim3(unsigned(nblk)), dim3(kThreads), 0, stream>>>(f);
+  e = hipGetLastError();
+  if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("finalize launch: ") + hipGetErrorString(e));
+  return DENDSN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,722 @@
+// DendSN layer scan kernels for gfx950 (CDNA4, wave64).
+//
+// One kernel per direction.  A neuron's B branches are held by L adjacent lanes
+// of one wavefront, BL = B / L branches per lane, so one time step of X for a
+// wave is one contiguous, fully coalesced stretch of [T, N, B] memory.  The
+// dendritic states stay in registers across the time loop; the only cross-lane
+// traffic is the branch-to-soma sum Z, reduced with DPP inside the L-lane group,
+// and every lane of the group then runs the soma redundantly (no broadcast).
+//
+// A block owns a tile of positions of one sample (see TileMode) and loops over a
+// group of batch items, so per-channel parameters are loaded once per lane and
+// parameter-gradient partials are summed in registers across those items.
+//
+// The forward kernel and the backward kernel's recompute of the forward call
+// the same inline step functions, so (compiled with -ffp-contract=off, explicit
+// fmaf and the raw v_exp_f32) they reproduce bit-identical states and spikes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dendsn_plan.h"
+
+namespace dendsn {
+
+typedef uint16_t bf16_t;  // bf16 storage
+
+// -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
+constexpr float kNegHalfLog2e = -0.721347520444481703680f;
+constexpr float kLog2e = 1.442695040888963407360f;
+constexpr float kPi = 3.141592653589793238463f;
+
+// ---------------------------------------------------------------------------
+// Storage conversions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Two floats -> two bf16 in one dword, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  f32x2_t f = {a, b};
+  bf16x2_t h = __builtin_convertvector(f, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, h);
+}
+__device__ __forceinline__ bf16_t to_bf16(float a) {
+  return __builtin_bit_cast(bf16_t, static_cast<__bf16>(a));
+}
+
+template <int BL>
+__device__ __forceinline__ void load_vec(const float* __restrict__ p, float (&v)[BL]) {
+  if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const float4 q = reinterpret_cast<const float4*>(p)[i];
+      v[4 * i] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const float2 q = reinterpret_cast<const float2*>(p)[i];
+      v[2 * i] = q.x; v[2 * i + 1] = q.y;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) v[i] = p[i];
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void load_vec(const bf16_t* __restrict__ p, float (&v)[BL]) {
+  if constexpr (BL % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 8; ++i) {
+      const uint4 q = reinterpret_cast<const uint4*>(p)[i];
+      v[8 * i + 0] = bf16_lo(q.x); v[8 * i + 1] = bf16_hi(q.x);
+      v[8 * i + 2] = bf16_lo(q.y); v[8 * i + 3] = bf16_hi(q.y);
+      v[8 * i + 4] = bf16_lo(q.z); v[8 * i + 5] = bf16_hi(q.z);
+      v[8 * i + 6] = bf16_lo(q.w); v[8 * i + 7] = bf16_hi(q.w);
+    }
+  } else if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const uint2 q = reinterpret_cast<const uint2*>(p)[i];
+      v[4 * i + 0] = bf16_lo(q.x); v[4 * i + 1] = bf16_hi(q.x);
+      v[4 * i + 2] = bf16_lo(q.y); v[4 * i + 3] = bf16_hi(q.y);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const uint32_t q = reinterpret_cast<const uint32_t*>(p)[i];
+      v[2 * i] = bf16_lo(q); v[2 * i + 1] = bf16_hi(q);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) v[i] = bf16_lo(p[i]);
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void store_vec(float* __restrict__ p, const float (&v)[BL]) {
+  if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i)
+      reinterpret_cast<float4*>(p)[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) reinterpret_cast<float2*>(p)[i] = make_float2(v[2 * i], v[2 * i + 1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) p[i] = v[i];
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void store_vec(bf16_t* __restrict__ p, const float (&v)[BL]) {
+  if constexpr (BL % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 8; ++i) {
+      uint4 q;
+      q.x = pack_bf16x2(v[8 * i + 0], v[8 * i + 1]);
+      q.y = pack_bf16x2(v[8 * i + 2], v[8 * i + 3]);
+      q.z = pack_bf16x2(v[8 * i + 4], v[8 * i + 5]);
+      q.w = pack_bf16x2(v[8 * i + 6], v[8 * i + 7]);
+      reinterpret_cast<uint4*>(p)[i] = q;
+    }
+  } else if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      uint2 q;
+      q.x = pack_bf16x2(v[4 * i + 0], v[4 * i + 1]);
+      q.y = pack_bf16x2(v[4 * i + 2], v[4 * i + 3]);
+      reinterpret_cast<uint2*>(p)[i] = q;
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) reinterpret_cast<uint32_t*>(p)[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) p[i] = to_bf16(v[i]);
+  }
+}
+
+// Address = wave-uniform base (scalar registers) + 32-bit per-lane byte offset.
+template <typename P>
+__device__ __forceinline__ P* at(P* base, uint32_t off) {
+  return reinterpret_cast<P*>(reinterpret_cast<char*>(base) + off);
+}
+template <typename P>
+__device__ __forceinline__ const P* at(const P* base, uint32_t off) {
+  return reinterpret_cast<const P*>(reinterpret_cast<const char*>(base) + off);
+}
+
+__device__ __forceinline__ float load_one(const float* p) { return *p; }
+__device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(*p); }
+__device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
+__device__ __forceinline__ void store_spike(bf16_t* p, bool s) { *p = s ? bf16_t(0x3f80) : bf16_t(0); }
+
+// ---------------------------------------------------------------------------
+// Cross-lane sum inside an L-lane group (L <= 16) with DPP.  Every lane of the
+// group ends with the same bits: each level adds a pair of partial sums that
+// both partners hold, and float addition is commutative.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+template <int L>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(L == 1 || L == 2 || L == 4 || L == 8 || L == 16, "L must be a power of two <= 16");
+  if constexpr (L >= 2) v += dpp_f32<0xb1>(v);   // quad_perm(1,0,3,2): partner lane ^ 1
+  if constexpr (L >= 4) v += dpp_f32<0x4e>(v);   // quad_perm(2,3,0,1): partner lane ^ 2
+  if constexpr (L >= 8) v += dpp_f32<0x141>(v);  // row_half_mirror: lane i <-> 7 - i in each 8
+  if constexpr (L >= 16) v += dpp_f32<0x140>(v); // row_mirror: lane i <-> 15 - i in each 16
+  return v;
+}
+
+// Pairwise tree over a lane's BL partial products (left fold for odd counts).
+template <int BL>
+__device__ __forceinline__ float lane_sum(const float (&p)[BL]) {
+  if constexpr (BL == 1) {
+    return p[0];
+  } else if constexpr (BL == 2) {
+    return p[0] + p[1];
+  } else if constexpr (BL == 4) {
+    return (p[0] + p[1]) + (p[2] + p[3]);
+  } else if constexpr (BL == 8) {
+    return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+  } else {
+    float s = p[0];
+#pragma unroll
+    for (int i = 1; i < BL; ++i) s += p[i];
+    return s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-lane branch parameters of one channel.
+// ---------------------------------------------------------------------------
+template <int BL>
+struct Branches {
+  float k[BL];   // kappa * m  (0 for a gated-off branch)
+  float xi[BL];
+  float rz[BL];  // 1 / zeta
+  bool on[BL];   // mask bit
+};
+
+template <int BL>
+__device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int sub, Branches<BL>& br) {
+  const int64_t base = c * a.B + int64_t(sub) * BL;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) {
+    const bool on = a.mask ? (a.mask[base + j] != 0) : true;
+    br.on[j] = on;
+    br.k[j] = on ? a.kappa[base + j] : 0.0f;
+    br.xi[j] = a.xi ? a.xi[base + j] : 0.0f;
+    br.rz[j] = a.zeta ? 1.0f / a.zeta[base + j] : 1.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// One forward step of the dendrite (leaky compartments, L2 aggregation with one
+// compartment per branch, activation, weighted branch sum) and of the LIF soma.
+// A gated-off branch keeps a zero state, so nothing it receives can reach the
+// soma or its gradients.
+// ---------------------------------------------------------------------------
+template <int BL, int L, int PSI>
+__device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv)[BL],
+                                               const Branches<BL>& br, float alpha,
+                                               float* efac = nullptr) {
+  float part[BL];
+#pragma unroll
+  for (int j = 0; j < BL; ++j) {
+    float v = fmaf(alpha, vd[j], xv[j]);   // alpha = 0: Stateless Dendrite
+    v = br.on[j] ? v : 0.0f;
+    vd[j] = v;
+    const float tt = (v - br.xi[j]) * br.rz[j];   // signed (Vd - xi)/zeta; u = |tt|
+    float y;
+    if constexpr (PSI == 1) {
+      const float q = tt * tt;
+      const float e = __builtin_amdgcn_exp2f(q * kNegHalfLog2e);
+      if (efac) efac[j] = e;
+      y = (1.0f - q) * e;
+    } else {
+      y = fabsf(tt);
+    }
+    part[j] = br.k[j] * y;
+  }
+  return group_sum<L>(lane_sum<BL>(part));
+}
+
+__device__ __forceinline__ void soma_step(float& h, bool& s, float z, float beta, float vth) {
+  h = s ? z : fmaf(beta, h, z);   // beta (1 - S[t-1]) H[t-1] + Z[t]
+  s = h >= vth;                   // Theta(H - v_th), Theta(0) = 1
+}
+
+// Surrogate derivative of Theta at x = H - v_th.
+__device__ __forceinline__ float surrogate(float x, int kind, float a) {
+  if (kind == 1) {  // a sigma(a x) (1 - sigma(a x)) = a e / (1 + e)^2, e = exp(-|a x|)
+    const float e = __builtin_amdgcn_exp2f(-fabsf(a * x) * kLog2e);
+    const float d = 1.0f + e;
+    return a * e * __builtin_amdgcn_rcpf(d * d);
+  }
+  const float px = kPi * x;  // 1 / (1 + pi^2 x^2)
+  return __builtin_amdgcn_rcpf(fmaf(px, px, 1.0f));
+}
+
+// ---------------------------------------------------------------------------
+// Where a thread sits: lane-in-neuron, position, batch way, group, channel.
+// ---------------------------------------------------------------------------
+struct Pos {
+  int sub, p, way, g;
+  int64_t c, m, tile;
+  bool active;
+};
+
+template <int L>
+__device__ __forceinline__ Pos locate(const ScanArgs& a) {
+  Pos r;
+  const int tid = threadIdx.x;
+  r.sub = tid % L;
+  const int q = tid / L;
+  r.p = q % a.pb;
+  // Batch ways are whole waves (kFC: pb * L == 64) or a single way, so the way
+  // index is wave-uniform; readfirstlane lets the compiler keep it scalar.
+  r.way = __builtin_amdgcn_readfirstlane(q / a.pb);
+  const int64_t blk = blockIdx.x;
+  r.tile = blk % a.ntiles;
+  r.g = int(blk / a.ntiles);
+  if (a.mode == kSpatial) {
+    const int64_t c = r.tile / a.tpc;
+    const int64_t s = (r.tile % a.tpc) * a.pb + r.p;
+    r.c = c;
+    r.active = s < a.S;
+    r.m = c * a.S + s;
+  } else {
+    const int64_t c = r.tile * a.cpt + r.p / a.S;
+    r.c = c;
+    r.active = (r.p < int64_t(a.cpt) * a.S) && (c < a.C);
+    r.m = c * a.S + r.p % a.S;
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Per-lane byte offsets of one neuron inside a sample's slice of a time row;
+// every other part of an address is wave-uniform (scalar registers).
+// ---------------------------------------------------------------------------
+struct LaneOff {
+  uint32_t x;   // X / grad_x element (I/O dtype)
+  uint32_t c;   // checkpointed dendritic state (fp32)
+  uint32_t s;   // spikes / grad_spikes (I/O dtype)
+  uint32_t v;   // fp32 per-neuron rows (v_soma, grad_v_soma, checkpointed H)
+};
+
+template <typename IO, int BL>
+__device__ __forceinline__ LaneOff lane_offsets(const ScanArgs& a, const Pos& pos) {
+  LaneOff o;
+  o.x = uint32_t((pos.m * a.B + pos.sub * BL) * int64_t(sizeof(IO)));
+  o.c = uint32_t((pos.m * a.B + pos.sub * BL) * 4);
+  o.s = uint32_t(pos.m * int64_t(sizeof(IO)));
+  o.v = uint32_t(pos.m * 4);
+  return o;
+}
+
+// Batch items of one lane: bt = first, first + ways, ... < end (wave-uniform).
+__device__ __forceinline__ int items_of(const ScanArgs& a, const Pos& pos, int64_t* first) {
+  *first = int64_t(pos.g) * a.bpg + pos.way;
+  const int64_t end = min(a.batch, int64_t(pos.g + 1) * a.bpg);
+  return *first < end ? int((end - *first + a.ways - 1) / a.ways) : 0;
+}
+
+// ---------------------------------------------------------------------------
+// Forward kernel.
+//
+// Each lane walks the rows X[t] of its neurons (one neuron per batch item) as
+// one stream, in chunks of D rows, double-buffered: chunk c+1 is in flight
+// while chunk c is computed.  A neuron's rows are padded to a multiple of D by
+// re-reading its last row; padded steps compute but store nothing, and the
+// state restarts at each neuron's first chunk.
+// ---------------------------------------------------------------------------
+template <typename IO, int BL, int D>
+struct RowCursor {  // wave-uniform position of the next chunk to load
+  const IO* base;   // X row 0 of the current neuron's batch item
+  int k, t;         // neuron index in the lane's list, first row of the chunk
+};
+
+template <typename IO, int BL, int D>
+__device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, D>& cur, uint32_t ox, int T,
+                                           int Tp, int64_t rowX, int64_t item_stride, float (&buf)[D][BL]) {
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    const int t = min(cur.t + k, T - 1);
+    load_vec<BL>(at(cur.base + int64_t(t) * rowX, ox), buf[k]);
+  }
+  cur.t += D;
+  if (cur.t >= Tp) {
+    cur.t = 0;
+    cur.k += 1;
+    cur.base += item_stride;
+  }
+}
+
+template <typename IO, int BL, int L, int PSI, int D>
+struct FwdLane {
+  // running state of the neuron being computed
+  float vd[BL];
+  float h;
+  bool s;
+  int t;          // step index of the chunk being computed
+  int64_t n0;     // first neuron of the current batch item (uniform)
+};
+
+template <typename IO, int BL, int L, int PSI, int D>
+__device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL>& br,
+                                              float alpha, bool lead, int T, int Tp, int64_t item_neurons,
+                                              const float (&buf)[D][BL], FwdLane<IO, BL, L, PSI, D>& st) {
+  const ScanArgs& a = fa.s;
+  const bool fresh = st.t == 0;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) st.vd[j] = fresh ? 0.0f : st.vd[j];
+  st.h = fresh ? 0.0f : st.h;
+  st.s = fresh ? false : st.s;
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    const int t = st.t + k;
+    const float z = dendrite_step<BL, L, PSI>(st.vd, buf[k], br, alpha);
+    soma_step(st.h, st.s, z, a.beta, a.vth);
+    if (t < T) {
+      const int64_t row = int64_t(t) * a.N + st.n0;
+      if (lead) {
+        store_spike(at(static_cast<IO*>(fa.spikes) + row, lo.s), st.s);
+        if (fa.vsoma) *at(fa.vsoma + row, lo.v) = st.h;
+      }
+      if (fa.ckpt && (t + 1) % a.K == 0 && t + 1 < T) {
+        const int64_t kk = (t + 1) / a.K - 1;
+        store_vec<BL>(at(fa.ckpt + (kk * a.N + st.n0) * a.B, lo.c), st.vd);
+        if (lead) *at(fa.ckpt + int64_t(a.nck) * a.N * a.B + kk * a.N + st.n0, lo.v) = st.h;
+      }
+    }
+  }
+  st.t += D;
+  if (st.t >= Tp) {
+    st.t = 0;
+    st.n0 += item_neurons;
+  }
+}
+
+template <typename IO, int BL, int L, int PSI>
+__global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
+  constexpr int D = 4;  // rows per chunk; two chunks in flight per lane
+  const ScanArgs& a = fa.s;
+  const Pos pos = locate<L>(a);
+  if (!pos.active) return;  // whole L-lane groups leave together
+  Branches<BL> br;
+  load_branches<BL>(a, pos.c, pos.sub, br);
+  const float alpha = a.alpha ? a.alpha[0] : 0.0f;
+  const LaneOff lo = lane_offsets<IO, BL>(a, pos);
+  const bool lead = pos.sub == 0;
+  const int T = int(a.T);
+  const int Tp = (T + D - 1) / D * D;
+  const int64_t rowX = a.N * a.B;
+  int64_t bt0;
+  const int nk = items_of(a, pos, &bt0);
+  const int nchunks = nk * (Tp / D);
+  const int64_t item_neurons = int64_t(a.ways) * a.M;
+
+  RowCursor<IO, BL, D> cur;
+  cur.base = static_cast<const IO*>(a.x) + bt0 * a.M * a.B;
+  cur.k = 0;
+  cur.t = 0;
+  FwdLane<IO, BL, L, PSI, D> st;
+  st.t = 0;
+  st.n0 = bt0 * a.M;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) st.vd[j] = 0.0f;
+  st.h = 0.0f;
+  st.s = false;
+
+  float bufA[D][BL], bufB[D][BL];
+  if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
+  for (int c = 0; c < nchunks; c += 2) {
+    if (c + 1 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufB);
+    compute_chunk<IO, BL, L, PSI, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
+    if (c + 2 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
+    if (c + 1 < nchunks) compute_chunk<IO, BL, L, PSI, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward kernel.  For each neuron, the segments between checkpoints are
+// visited from last to first.  A segment is cut into whole chunks of
+// compile-time length (KS, then powers of two for the remainder); a chunk
+// re-runs the forward from the segment's checkpoint up to its first step (only
+// chunks after the first need that), recomputes its own steps while stashing
+// the dendritic state and H in registers, then runs the adjoint recurrences
+// backwards through them.
+// ---------------------------------------------------------------------------
+template <int BL>
+struct Accum {
+  float k[BL], xi[BL], z[BL];
+  float a;
+};
+
+template <typename IO, int BL>
+struct BwdLane {  // adjoint state carried backwards through time, and pointers
+  float dh_next;
+  float lam[BL];
+  const IO* xbase;   // X of this batch item (uniform)
+  IO* gxbase;
+  const IO* gsbase;
+  const float* gvbase;
+};
+
+template <typename IO, int BL, int L, int PSI, int CS>
+__device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+                                          float alpha, float beta_r, int c0, const float (&v0)[BL], float h0,
+                                          bool s0, BwdLane<IO, BL>& bl, Accum<BL>& acc) {
+  const ScanArgs& a = ba.s;
+  const int64_t rowX = a.N * a.B;
+  const float beta = a.beta, vth = a.vth;
+  float xb[CS][BL];
+  float gsb[CS];
+#pragma unroll
+  for (int k = 0; k < CS; ++k) {
+    const int64_t t = c0 + k;
+    load_vec<BL>(at(bl.xbase + t * rowX, lo.x), xb[k]);
+    gsb[k] = load_one(at(bl.gsbase + t * a.N, lo.s));
+  }
+  // Recompute the chunk's steps exactly as the forward did (same inline step
+  // function); stash Vd, H and, for the Mexican hat, its exp(-u^2/2) factor.
+  float stv[CS + 1][BL];
+  float ste[PSI == 1 ? CS : 1][BL];
+  float sth[CS];
+#pragma unroll
+  for (int j = 0; j < BL; ++j) stv[0][j] = v0[j];
+  {
+    float h = h0;
+    bool s = s0;
+#pragma unroll
+    for (int k = 0; k < CS; ++k) {
+#pragma unroll
+      for (int j = 0; j < BL; ++j) stv[k + 1][j] = stv[k][j];
+      const float z = dendrite_step<BL, L, PSI>(stv[k + 1], xb[k], br, alpha, PSI == 1 ? ste[PSI == 1 ? k : 0] : nullptr);
+      soma_step(h, s, z, beta, vth);
+      sth[k] = h;
+    }
+  }
+  // Adjoint recurrences, last step first.
+#pragma unroll
+  for (int k = CS - 1; k >= 0; --k) {
+    const float hk = sth[k];
+    const bool sk = hk >= vth;
+    const float gv = bl.gvbase ? *at(bl.gvbase + int64_t(c0 + k) * a.N, lo.v) : 0.0f;
+    const float sgv = surrogate(hk - vth, ba.sg, ba.sg_scale);
+    const float dS = fmaf(-beta_r * hk, bl.dh_next, gsb[k]);  // beta_r = 0: reset detached
+    float dh = fmaf(sgv, dS, gv);
+    dh = sk ? dh : fmaf(beta, bl.dh_next, dh);
+    float gxo[BL];
+#pragma unroll
+    for (int j = 0; j < BL; ++j) {
+      const float tt = (stv[k + 1][j] - br.xi[j]) * br.rz[j];
+      float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
+      if constexpr (PSI == 1) {
+        const float q = tt * tt;
+        const float e = ste[PSI == 1 ? k : 0][j];
+        y = (1.0f - q) * e;
+        dps = tt * (q - 3.0f) * e;
+      } else {
+        y = fabsf(tt);
+        dps = tt > 0.0f ? 1.0f : (tt < 0.0f ? -1.0f : 0.0f);
+      }
+      const float r = (br.k[j] * dh) * dps * br.rz[j];
+      bl.lam[j] = fmaf(alpha, bl.lam[j], r);
+      gxo[j] = bl.lam[j];
+      acc.k[j] = fmaf(dh, y, acc.k[j]);
+      acc.xi[j] -= r;
+      acc.z[j] = fmaf(-r, tt, acc.z[j]);
+      acc.a = fmaf(bl.lam[j], stv[k][j], acc.a);
+    }
+    store_vec<BL>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
+    bl.dh_next = dh;
+  }
+}
+
+// Runs the forward from (vd, h, s) at step t_from up to (not including) t_to.
+template <typename IO, int BL, int L, int PSI>
+__device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, const Branches<BL>& br,
+                                        float alpha, const IO* xbase, int t_from, int t_to, float (&vd)[BL],
+                                        float& h, bool& s) {
+  const int64_t rowX = a.N * a.B;
+  for (int t = t_from; t < t_to; ++t) {
+    float xv[BL];
+    load_vec<BL>(at(xbase + int64_t(t) * rowX, lo.x), xv);
+    const float z = dendrite_step<BL, L, PSI>(vd, xv, br, alpha);
+    soma_step(h, s, z, a.beta, a.vth);
+  }
+}
+
+template <typename IO, int BL, int L, int PSI, int KS>
+__device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff& lo, int64_t bt,
+                                                const Branches<BL>& br, float alpha, Accum<BL>& acc) {
+  const ScanArgs& a = ba.s;
+  const int T = int(a.T);
+  const int K = a.K;
+  const float vth = a.vth;
+  const float beta_r = ba.detach ? 0.0f : a.beta;
+  const int64_t n0 = bt * a.M;  // first neuron of this batch item (wave-uniform)
+  BwdLane<IO, BL> bl;
+  bl.xbase = static_cast<const IO*>(a.x) + n0 * a.B;
+  bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.B;
+  bl.gsbase = static_cast<const IO*>(ba.gspk) + n0;
+  bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
+  bl.dh_next = 0.0f;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) bl.lam[j] = 0.0f;
+
+  const int nseg = (T + K - 1) / K;
+  for (int seg = nseg - 1; seg >= 0; --seg) {
+    const int t0 = seg * K;
+    const int t1 = min(T, t0 + K);
+    float vs[BL];
+    float hs = 0.0f;
+    if (seg == 0) {
+#pragma unroll
+      for (int j = 0; j < BL; ++j) vs[j] = 0.0f;
+    } else {
+      load_vec<BL>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.B, lo.c), vs);
+      hs = *at(ba.ckpt + int64_t(a.nck) * a.N * a.B + int64_t(seg - 1) * a.N + n0, lo.v);
+    }
+    const bool ss = (seg > 0) && (hs >= vth);
+    // Chunks: full KS-step chunks from t0, then the remainder in descending
+    // powers of two; visited from the last one back to t0.
+    const int len = t1 - t0;
+    const int nfull = len / KS;
+    const int rem = len - nfull * KS;
+    int end = t1;
+#pragma unroll
+    for (int cs = KS / 2; cs >= 1; cs /= 2) {
+      if (rem & cs) {
+        // This piece is the highest-placed remainder chunk not yet visited: it
+        // sits just below `end`.
+        const int c0 = end - cs;
+        float v[BL];
+#pragma unroll
+        for (int j = 0; j < BL; ++j) v[j] = vs[j];
+        float h = hs;
+        bool s = ss;
+        advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+        if constexpr (KS / 2 >= 1) {
+          if (cs == 8) bwd_chunk<IO, BL, L, PSI, (KS >= 16 ? 8 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
+          else if (cs == 4) bwd_chunk<IO, BL, L, PSI, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
+          else if (cs == 2) bwd_chunk<IO, BL, L, PSI, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
+          else bwd_chunk<IO, BL, L, PSI, 1>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
+        }
+        end = c0;
+      }
+    }
+    for (int ch = nfull - 1; ch >= 0; --ch) {
+      const int c0 = t0 + ch * KS;
+      float v[BL];
+#pragma unroll
+      for (int j = 0; j < BL; ++j) v[j] = vs[j];
+      float h = hs;
+      bool s = ss;
+      advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+      bwd_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
+    }
+  }
+}
+
+// Block reduction of the parameter-gradient partials, in a fixed order.
+template <int BL, int L>
+__device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& pos, Accum<BL>& acc) {
+  const ScanArgs& a = ba.s;
+  __shared__ float red[kThreads * BL];
+  __shared__ float reda[kThreads / 64];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int B = a.B;
+
+  float va = acc.a;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) va += __shfl_xor(va, off);
+  if (lane == 0) reda[wave] = va;
+
+  if (a.mode == kSpatial) {
+    // One channel per block: sum lanes of equal sub within the wave, then waves.
+    const int64_t c = pos.c;
+    const int64_t jt = pos.tile % a.tpc;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+#pragma unroll
+      for (int j = 0; j < BL; ++j) {
+        float v = q == 0 ? acc.k[j] : (q == 1 ? acc.xi[j] : acc.z[j]);
+#pragma unroll
+        for (int off = 32; off >= L; off >>= 1) v += __shfl_xor(v, off);
+        if (lane < L) red[((q * BL + j) * 4 + wave) * L + lane] = v;
+      }
+    }
+    __syncthreads();
+    for (int o = tid; o < 3 * B; o += kThreads) {
+      const int q = o / B, b = o % B;
+      const int sub = b / BL, j = b % BL;
+      float s = 0.0f;
+      for (int w = 0; w < 4; ++w) s += red[((q * BL + j) * 4 + w) * L + sub];
+      ba.wsP[((int64_t(pos.g) * a.C + c) * a.tpc + jt) * 3 * B + q * B + b] = s;
+    }
+  } else {
+    // Whole channels per tile: sum the batch ways and the S positions of each channel.
+    for (int q = 0; q < 3; ++q) {
+#pragma unroll
+      for (int j = 0; j < BL; ++j)
+        red[tid * BL + j] = q == 0 ? acc.k[j] : (q == 1 ? acc.xi[j] : acc.z[j]);
+      __syncthreads();
+      for (int o = tid; o < a.cpt * B; o += kThreads) {
+        const int slot = o / B, b = o % B;
+        const int64_t c = pos.tile * a.cpt + slot;
+        if (c >= a.C) continue;
+        const int sub = b / BL, j = b % BL;
+        float s = 0.0f;
+        for (int w = 0; w < a.ways; ++w)
+          for (int sp = 0; sp < a.S; ++sp) {
+            const int thr = (w * a.pb + slot * int(a.S) + sp) * L + sub;
+            s += red[thr * BL + j];
+          }
+        ba.wsP[(int64_t(pos.g) * a.C + c) * 3 * B + q * B + b] = s;
+      }
+      __syncthreads();
+    }
+  }
+  __syncthreads();
+  if (tid == 0) ba.wsA[int64_t(pos.g) * a.ntiles + pos.tile] = (reda[0] + reda[1]) + (reda[2] + reda[3]);
+}
+
+template <typename IO, int BL, int L, int PSI, int KS>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * KS <= 16 ? 3 : 2))) dendsn_bwd_kernel(BwdArgs ba) {
+  const ScanArgs& a = ba.s;
+  const Pos pos = locate<L>(a);
+  Accum<BL> acc;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) acc.k[j] = acc.xi[j] = acc.z[j] = 0.0f;
+  acc.a = 0.0f;
+  if (pos.active) {
+    Branches<BL> br;
+    load_branches<BL>(a, pos.c, pos.sub, br);
+    const float alpha = a.alpha ? a.alpha[0] : 0.0f;
+    const LaneOff lo = lane_offsets<IO, BL>(a, pos);
+    int64_t bt0;
+    const int nk = items_of(a, pos, &bt0);
+    for (int i = 0; i < nk; ++i) backward_neuron<IO, BL, L, PSI, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
+  }
+  reduce_partials<BL, L>(ba, pos, acc);
+}
+
+// Fixed-order float64 sum of the partials into the parameter gradients; the
+// last block reduces g_alpha.
+__global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f);
+
+}  // namespace dendsn

@@ -1,0 +1,90 @@
+// Launch plan and kernel argument blocks shared by the host API and the kernel
+// translation units.  Plain data only: no HIP runtime calls here.
+#pragma once
+
+#include <stdint.h>
+
+namespace dendsn {
+
+constexpr int kThreads = 256;  // 4 wave64s per block
+
+// How the positions m = c * S + s of one sample are cut into per-block tiles.
+// Tiles never straddle a channel unless they hold whole channels, so a block's
+// parameter-gradient partials belong to a known set of channels.
+enum TileMode : int32_t {
+  kSpatial = 0,  // S >= positions per block: a tile is pb positions of ONE channel
+  kFC = 1,       // S == 1: a tile is pb channels; the 4 waves split the batch items
+  kSeg = 2,      // 1 < S < pb: a tile is cpt whole channels of S positions
+};
+
+struct Plan {
+  int32_t BL;     // branches held by one lane
+  int32_t L;      // lanes per neuron (power of two, <= 16); B = BL * L
+  int32_t fast;   // 1: a vector-width mapping with every stash capacity compiled
+  int32_t mode;   // TileMode
+  int32_t ways;   // batch ways inside a block (waves that share positions)
+  int32_t pb;     // positions per way in a block; pb * L * ways == kThreads
+  int32_t tpc;    // tiles per channel (kSpatial), else 1
+  int32_t cpt;    // channels per tile (kFC / kSeg), else 1
+  int64_t ntiles; // tiles per sample
+  int32_t G;      // batch groups (grid = ntiles * G blocks)
+  int32_t bpg;    // batch items per group
+  int32_t KS;     // backward stash capacity in steps (compile-time in the kernel)
+  int32_t nck;    // interior checkpoints, ceil(T / K) - 1
+};
+
+struct ScanArgs {
+  const void* x;
+  const float* alpha;   // NULL for the Stateless Dendrite (alpha = 0)
+  const float* kappa;
+  const float* xi;      // NULL: 0
+  const float* zeta;    // NULL: 1
+  const uint8_t* mask;  // NULL: all branches kept
+  int64_t T, N, C, S, M, batch;  // M = C * S positions per sample
+  int32_t B, K, nck;
+  float beta, vth;
+  int32_t mode, ways, pb, tpc, cpt, bpg;
+  int64_t ntiles;
+};
+
+struct FwdArgs {
+  ScanArgs s;
+  void* spikes;
+  float* vsoma;  // optional
+  float* ckpt;   // optional; [nck][N][B] dendritic state then [nck][N] somatic potential
+};
+
+struct BwdArgs {
+  ScanArgs s;
+  const float* ckpt;
+  const void* gspk;
+  const float* gv;  // optional
+  void* gx;
+  float* wsP;       // [G][C][tpc][3][B] partial sums of (g_kappa, g_xi, g_zeta)
+  float* wsA;       // [G][ntiles] partial sums of g_alpha
+  int32_t detach;
+  int32_t sg;
+  float sg_scale;
+};
+
+struct FinArgs {
+  const float* wsP;
+  const float* wsA;
+  const uint8_t* mask;
+  float* gk;
+  float* gxi;
+  float* gz;
+  float* ga;
+  int64_t C, nA;
+  int32_t B, G, tpc, stateful;
+};
+
+// Compiled (BL, L) mappings.  "Fast" mappings move 8 or 16 bytes per lane;
+// "generic" ones cover other branch counts.  Backward stash capacities: 4 steps
+// for every mapping, and 8 steps too when a lane holds at most 4 branches.
+#define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
+#define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
+#define DENDSN_GENERIC(X) X(1, 1) X(2, 1) X(3, 1) X(5, 1) X(6, 1) X(7, 1) X(5, 2) X(6, 2) X(7, 2)
+#define DENDSN_GENERIC_KS 4
+
+}  // namespace dendsn

@@ -1,0 +1,214 @@
+"""Parity harness: run the HIP library and the float64 oracle on the same
+seeded inputs and compare them element by element.
+
+Spike protocol.  A spike is a floating-point decision (H - v_th >= 0) that the
+kernel takes in fp32 and the oracle in fp64.  Spikes must agree exactly,
+except at events whose oracle potential lies within ``band`` (1e-6) of the
+threshold.  Each such event is resolved by re-running the oracle with the
+kernel's decision imposed at that step (the oracle then follows the same spike
+train), repeating until no disagreement is left; every exemption is counted and
+reported.  A disagreement outside the band fails.
+
+Tolerances.  fp32 outputs: |g - o| <= rtol (|o| + rms(o)) elementwise, rms over
+the tensor; summed parameter gradients: |g - o| <= rtol * sum|terms|.
+rtol is 1e-5 for fp32 results and 2e-2 for results stored in bf16.
+"""
+
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass, field
+
+import numpy as np
+
+import oracle
+
+BAND = 1e-6
+RTOL_F32 = 1e-5
+RTOL_BF16 = 2e-2
+
+
+def announce(msg: str):
+    """Name the case before a GPU step, past pytest's capture, flushed."""
+    sys.__stderr__.write(f"[gpu] {msg}\n")
+    sys.__stderr__.flush()
+
+
+@dataclass
+class Case:
+    """One parity case: a layer config and its seeded inputs (host, float32)."""
+
+    cfg: object                      # paper_2412_06355_amd.DendSNConfig
+    X: np.ndarray                    # [T, N, B] float32 (already bf16-representable for bf16)
+    gS: np.ndarray                   # [T, N] float32
+    kappa: np.ndarray
+    xi: np.ndarray | None
+    zeta: np.ndarray | None
+    mask: np.ndarray | None
+    alpha: float
+    gV: np.ndarray | None = None
+    name: str = ""
+
+
+@dataclass
+class Report:
+    exemptions: int = 0
+    max_err: dict = field(default_factory=dict)
+
+    def __str__(self):
+        errs = ", ".join(f"{k}={v:.2e}" for k, v in self.max_err.items())
+        return f"exemptions={self.exemptions} {errs}"
+
+
+def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True, mask_rho=None,
+              with_gv=False, name=""):
+    """Seeded inputs for a config (numpy PCG64).  bf16 storage is emulated by
+    rounding the float32 draws to bf16 (round to nearest even) with torch."""
+    import torch
+
+    rng = np.random.default_rng(seed)
+    T, N, B, C = cfg.T, cfg.N, cfg.B, cfg.C
+    X = rng.normal(x_mean, x_std, size=(T, N, B)).astype(np.float32)
+    gS = rng.normal(size=(T, N)).astype(np.float32)
+    if cfg.io == "bf16":
+        X = torch.from_numpy(X).to(torch.bfloat16).float().numpy()
+        gS = torch.from_numpy(gS).to(torch.bfloat16).float().numpy()
+    kappa = rng.uniform(0.0, 1.0, size=(C, B)).astype(np.float32)
+    if random_affine:
+        xi = rng.normal(0.0, 0.5, size=(C, B)).astype(np.float32)
+        zeta = rng.uniform(0.5, 2.0, size=(C, B)).astype(np.float32)
+    else:
+        xi = zeta = None
+    mask = (rng.random((C, B)) < mask_rho).astype(np.uint8) if mask_rho is not None else None
+    gV = rng.normal(size=(T, N)).astype(np.float32) if with_gv else None
+    return Case(cfg=cfg, X=X, gS=gS, kappa=kappa, xi=xi, zeta=zeta, mask=mask, alpha=alpha, gV=gV, name=name)
+
+
+# ---------------------------------------------------------------------------
+# GPU side
+# ---------------------------------------------------------------------------
+def to_device(case: Case, device):
+    import torch
+
+    io = torch.bfloat16 if case.cfg.io == "bf16" else torch.float32
+    t = lambda a, dt=torch.float32: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(
+        device=device, dtype=dt)
+    return dict(
+        x=t(case.X, io), gS=t(case.gS, io), gV=t(case.gV),
+        alpha=torch.tensor([case.alpha], dtype=torch.float32, device=device),
+        kappa=t(case.kappa), xi=t(case.xi), zeta=t(case.zeta),
+        mask=None if case.mask is None else torch.from_numpy(case.mask).to(device),
+    )
+
+
+def run_gpu(case: Case, device, dev=None, want_v_soma=True):
+    """Forward + backward through the C ABI.  Returns float64 numpy results."""
+    import torch
+
+    import paper_2412_06355_amd as dendsn
+
+    announce(f"case {case.name or '?'}: {case.cfg}")
+    d = dev if dev is not None else to_device(case, device)
+    spikes, v_soma, ckpt = dendsn.forward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"],
+                                          d["mask"], want_v_soma=want_v_soma)
+    g = dendsn.backward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"], ckpt,
+                        d["gS"], d["gV"])
+    torch.cuda.synchronize(device)
+    f = lambda t: None if t is None else t.float().cpu().numpy().astype(np.float64)
+    return dict(S=f(spikes), H=f(v_soma), gX=f(g["grad_x"]), g_alpha=float(g["grad_alpha"].item()),
+                g_kappa=f(g["grad_kappa"]), g_xi=f(g["grad_xi"]), g_zeta=f(g["grad_zeta"]),
+                raw=dict(spikes=spikes, v_soma=v_soma, grads=g))
+
+
+# ---------------------------------------------------------------------------
+# Oracle side and comparison
+# ---------------------------------------------------------------------------
+def run_oracle(case: Case, force=None):
+    cfg = case.cfg
+    rec = oracle.forward(
+        case.X.astype(np.float64), alpha=case.alpha if cfg.stateful else 0.0, beta=cfg.beta, v_th=cfg.v_th,
+        kappa=case.kappa, xi=case.xi, zeta=case.zeta, mask=case.mask, C=cfg.C, S=cfg.S,
+        psi_kind=cfg.psi, stateful=cfg.stateful, force=force)
+    return rec
+
+
+def oracle_grads(case: Case, rec):
+    cfg = case.cfg
+    return oracle.backward(rec, case.gS.astype(np.float64),
+                           None if case.gV is None else case.gV.astype(np.float64),
+                           sg_kind=cfg.sg, sg_scale=cfg.sg_scale, detach_reset=cfg.detach_reset)
+
+
+def resolve_spikes(case: Case, S_gpu: np.ndarray, band: float = BAND):
+    """Forced-spike protocol.  Returns (oracle record, number of exemptions)."""
+    T, N = S_gpu.shape
+    force = -np.ones((T, N), dtype=np.int64)
+    exempt = 0
+    for _ in range(T + 1):
+        rec = run_oracle(case, force if exempt else None)
+        diff = rec["S"] != S_gpu
+        if not diff.any():
+            return rec, exempt
+        # earliest disagreement of each neuron
+        cols = np.nonzero(diff.any(axis=0))[0]
+        t_first = diff[:, cols].argmax(axis=0)
+        dist = np.abs(rec["H"][t_first, cols] - cfg_vth(case))
+        bad = dist > band
+        if bad.any():
+            i = int(np.argmax(bad))
+            raise AssertionError(
+                f"spike mismatch outside the {band:g} band at t={t_first[i]}, n={cols[i]}: "
+                f"oracle H={rec['H'][t_first[i], cols[i]]!r}, gpu S={S_gpu[t_first[i], cols[i]]}")
+        force[t_first, cols] = S_gpu[t_first, cols].astype(np.int64)
+        exempt += len(cols)
+    raise AssertionError("forced-spike protocol did not converge")
+
+
+def cfg_vth(case):
+    return case.cfg.v_th
+
+
+def close_elementwise(name, g, o, rtol, report: Report):
+    scale = np.abs(o) + np.sqrt(np.mean(o * o)) if o.size else np.abs(o)
+    err = np.abs(g - o)
+    ratio = float(np.max(err / np.maximum(scale, 1e-300))) if o.size else 0.0
+    report.max_err[name] = ratio
+    if not np.all(err <= rtol * scale):
+        i = np.unravel_index(np.argmax(err - rtol * scale), o.shape)
+        raise AssertionError(f"{name}: |gpu - oracle| too large at {i}: gpu={g[i]!r} oracle={o[i]!r} "
+                             f"(max err/scale {ratio:.3e}, rtol {rtol:g})")
+
+
+def close_summed(name, g, o, absum, rtol, report: Report):
+    g, o, absum = np.asarray(g, np.float64), np.asarray(o, np.float64), np.asarray(absum, np.float64)
+    err = np.abs(g - o)
+    scale = np.maximum(absum, 1e-30)
+    report.max_err[name] = float(np.max(err / scale)) if err.size else 0.0
+    if not np.all(err <= rtol * scale):
+        i = np.unravel_index(np.argmax(err - rtol * scale), np.shape(o)) if np.ndim(o) else ()
+        raise AssertionError(f"{name}: gpu={np.asarray(g)[i]!r} oracle={np.asarray(o)[i]!r} "
+                             f"abs-sum={np.asarray(absum)[i]!r} rtol={rtol:g}")
+
+
+def compare(case: Case, gpu: dict) -> Report:
+    cfg = case.cfg
+    rep = Report()
+    rec, rep.exemptions = resolve_spikes(case, gpu["S"])
+    assert np.array_equal(gpu["S"], rec["S"])
+    assert set(np.unique(gpu["S"])).issubset({0.0, 1.0})
+    og = oracle_grads(case, rec)
+    if gpu["H"] is not None:
+        close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, rep)
+    rt_io = RTOL_BF16 if cfg.io == "bf16" else RTOL_F32
+    close_elementwise("grad_x", gpu["gX"], og["gX"], rt_io, rep)
+    for k in ("g_kappa", "g_xi", "g_zeta"):
+        close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, rep)
+    close_summed("g_alpha", gpu["g_alpha"], og["g_alpha"] if cfg.stateful else 0.0,
+                 og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, rep)
+    if case.mask is not None:
+        off = case.mask == 0
+        for k in ("g_kappa", "g_xi", "g_zeta"):
+            assert np.all(gpu[k][off] == 0.0), k
+        cidx = (np.arange(cfg.N) // cfg.S) % cfg.C
+        assert np.all(gpu["gX"][:, off[cidx]] == 0.0)
+    return rep

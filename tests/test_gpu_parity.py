@@ -1,0 +1,217 @@
+"""GPU parity: the HIP library (through the C ABI) against the float64 oracle,
+element by element, on seeded inputs (see tests/parity.py for the protocol).
+
+Sizes are ones the oracle finishes in seconds, chosen to span several tiles,
+every tiling mode (spatial tiles, fully connected tiles, multi-channel tiles),
+every lane mapping, ragged tails in space, batch and time, and chunked /
+checkpointed backward segments.
+"""
+
+import zlib
+
+import numpy as np
+import pytest
+
+import paper_2412_06355_amd as dendsn
+from tests.parity import announce, compare, make_case, run_gpu, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def cfg(**kw):
+    base = dict(T=4, batch=2, C=256, S=1, B=4, beta=0.5, v_th=1.0, psi="mexhat", sg="sigmoid", sg_scale=4.0)
+    base.update(kw)
+    return dendsn.DendSNConfig(**base)
+
+
+# --- the tiny layer: T=4, batch 2, 256 neurons, 4 branches, X ~ N(0,1) seed 0 ---
+@pytest.mark.parametrize("psi", ["mexhat", "identity"])
+@pytest.mark.parametrize("sg", ["sigmoid", "atan"])
+@pytest.mark.parametrize("detach", [False, True])
+def test_tiny_layer(gpu_device, psi, sg, detach):
+    c = cfg(psi=psi, sg=sg, detach_reset=detach)
+    case = make_case(c, seed=0, random_affine=False, name=f"tiny/{psi}/{sg}/detach={detach}")
+    rep = compare(case, run_gpu(case, gpu_device))
+    print(rep)
+
+
+def test_tiny_layer_with_grad_v_soma(gpu_device):
+    case = make_case(cfg(), seed=1, with_gv=True, name="tiny/gV")
+    compare(case, run_gpu(case, gpu_device))
+
+
+# --- shapes covering tiling modes, lane mappings and ragged tails ---
+SHAPES = [
+    # T, batch, C, S, B, io, K
+    (1, 3, 5, 1, 1, "f32", 1),
+    (2, 2, 3, 7, 2, "f32", 2),
+    (3, 1, 4, 300, 3, "f32", 3),
+    (5, 3, 6, 5, 5, "bf16", 2),
+    (7, 2, 9, 64, 6, "f32", 3),
+    (9, 2, 3, 130, 7, "f32", 4),
+    (6, 5, 11, 1, 10, "f32", 6),
+    (5, 2, 7, 3, 12, "bf16", 5),
+    (4, 3, 70, 1, 16, "f32", 4),
+    (4, 2, 40, 1, 32, "f32", 4),
+    (4, 2, 20, 1, 64, "f32", 2),
+    (3, 2, 8, 1, 128, "bf16", 3),
+    (4, 3, 5, 513, 8, "bf16", 4),
+    (4, 2, 3, 257, 4, "bf16", 4),
+    (11, 2, 3, 33, 4, "f32", 5),
+    (17, 2, 9, 1, 16, "f32", 17),
+    (20, 2, 5, 1, 4, "f32", 20),
+    (16, 3, 3, 2, 8, "f32", 16),
+    (13, 2, 6, 1, 8, "bf16", 13),
+    (10, 2, 4, 100, 2, "f32", 10),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}{}K{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "id-atan-stateless", "mh-atan-detach"])
+def test_shapes(gpu_device, shape, variant):
+    T, batch, C, S, B, io, K = shape
+    psi = "mexhat" if variant.startswith("mh") else "identity"
+    sg = "sigmoid" if "sig" in variant else "atan"
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, io=io, ckpt_every=K, psi=psi, sg=sg,
+            stateful="stateless" not in variant, detach_reset="detach" in variant, beta=0.7)
+    seed = zlib.crc32(repr((shape, variant)).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6,
+                     mask_rho=0.5 if "mask" in variant else None, name=f"{shape}/{variant}")
+    compare(case, run_gpu(case, gpu_device))
+
+
+# --- the benchmark layer shapes with the batch cut down (every other size kept) ---
+REDUCED = {
+    "cifar": dict(T=4, batch=2, C=128, S=1024, B=8, x_std=0.5),
+    "imagenet_stem": dict(T=4, batch=1, C=64, S=12544, B=4, io="bf16"),
+    "long_horizon": dict(T=64, batch=2, C=4096, S=1, B=16, x_mean=0.1, alpha=0.8, beta=0.9, ckpt_every=8),
+    "dbg": dict(T=4, batch=2, C=8192, S=1, B=32, mask_rho=0.5),
+}
+
+
+@pytest.mark.parametrize("name", list(REDUCED))
+def test_reduced_workloads(gpu_device, name):
+    kw = dict(REDUCED[name])
+    x_mean, x_std = kw.pop("x_mean", 0.0), kw.pop("x_std", 1.0)
+    alpha, rho = kw.pop("alpha", 0.5), kw.pop("mask_rho", None)
+    c = cfg(**kw)
+    case = make_case(c, seed=7, x_mean=x_mean, x_std=x_std, alpha=alpha, random_affine=False,
+                     mask_rho=rho, name=f"reduced/{name}")
+    rep = compare(case, run_gpu(case, gpu_device))
+    print(name, rep)
+
+
+# --- invariants that must hold bit for bit on the GPU ---
+def _bits(t):
+    import torch
+
+    return t.contiguous().view(torch.uint8)
+
+
+def test_checkpoint_interval_is_bit_invariant(gpu_device):
+    import torch
+
+    base = cfg(T=64, batch=2, C=512, S=1, B=16, beta=0.9, ckpt_every=8)
+    case = make_case(base, seed=11, x_mean=0.1, alpha=0.8, random_affine=True, mask_rho=0.7, name="ckpt8")
+    d = to_device(case, gpu_device)
+    outs = []
+    for K in (8, 64, 5, 1):
+        case.cfg = base.with_(ckpt_every=K)
+        announce(f"ckpt interval K={K}")
+        g = run_gpu(case, gpu_device, dev=d)["raw"]
+        outs.append(g)
+    ref = outs[0]
+    for o in outs[1:]:
+        assert torch.equal(o["spikes"], ref["spikes"])
+        assert torch.equal(o["v_soma"], ref["v_soma"])
+        assert torch.equal(_bits(o["grads"]["grad_x"]), _bits(ref["grads"]["grad_x"]))
+
+
+def test_run_to_run_determinism(gpu_device):
+    import torch
+
+    case = make_case(cfg(T=6, batch=5, C=64, S=300, B=8), seed=12, mask_rho=0.5, name="determinism")
+    d = to_device(case, gpu_device)
+    a = run_gpu(case, gpu_device, dev=d)["raw"]
+    b = run_gpu(case, gpu_device, dev=d)["raw"]
+    assert torch.equal(a["spikes"], b["spikes"])
+    for k in a["grads"]:
+        assert torch.equal(_bits(a["grads"][k]), _bits(b["grads"][k])), k
+
+
+def test_mask_of_ones_equals_no_mask(gpu_device):
+    import torch
+
+    case = make_case(cfg(T=5, batch=3, C=96, S=1, B=32), seed=13, name="mask-ones")
+    d = to_device(case, gpu_device)
+    a = run_gpu(case, gpu_device, dev=d)["raw"]
+    d["mask"] = torch.ones((96, 32), dtype=torch.uint8, device=gpu_device)
+    case.mask = np.ones((96, 32), np.uint8)
+    b = run_gpu(case, gpu_device, dev=d)["raw"]
+    assert torch.equal(a["spikes"], b["spikes"])
+    for k in a["grads"]:
+        assert torch.equal(_bits(a["grads"][k]), _bits(b["grads"][k])), k
+
+
+def test_masked_branches_get_exact_positive_zero(gpu_device):
+    case = make_case(cfg(T=4, batch=2, C=64, S=3, B=8), seed=14, mask_rho=0.5, name="mask-zero")
+    # gated-off branches receive inf / nan inputs: nothing may leak out of them
+    cidx = (np.arange(case.cfg.N) // case.cfg.S) % case.cfg.C
+    off = (case.mask == 0)[cidx]
+    case.X[:, off] = np.where(np.random.default_rng(0).random(case.X[:, off].shape) < 0.5, np.inf, np.nan)
+    g = run_gpu(case, gpu_device)
+    assert not np.any(np.signbit(g["gX"][:, off])) and np.all(g["gX"][:, off] == 0)
+    for k in ("g_kappa", "g_xi", "g_zeta"):
+        assert np.all(g[k][case.mask == 0] == 0) and not np.any(np.signbit(g[k][case.mask == 0]))
+    assert np.all(np.isfinite(g["gX"])) and np.isfinite(g["g_alpha"])
+    case.X[:, off] = 0.0
+    compare(case, g)
+
+
+def test_lif_reduction(gpu_device):
+    """B = 1, identity, kappa = 1, xi = 0, zeta = 1, alpha = 0, X >= 0: a LIF neuron."""
+    c = cfg(T=32, batch=4, C=300, S=1, B=1, psi="identity", beta=0.9, stateful=False)
+    case = make_case(c, seed=15, random_affine=False, name="lif")
+    case.X = np.abs(case.X)
+    case.kappa = np.ones_like(case.kappa)
+    g = run_gpu(case, gpu_device)
+    x = case.X[:, :, 0].astype(np.float64)
+    v = np.zeros(c.N)
+    s = np.zeros(c.N)
+    for t in range(c.T):
+        v = 0.9 * (1 - s) * v + x[t]
+        s = (v >= 1.0).astype(np.float64)
+        near = np.abs(v - 1.0) <= 1e-6
+        assert np.all((g["S"][t] == s) | near)
+        s = np.where(near, g["S"][t], s)
+        assert np.allclose(g["H"][t], v, rtol=1e-6, atol=1e-7)
+
+
+def test_batch_grouping_changes_nothing_but_rounding(gpu_device):
+    import torch
+
+    base = cfg(T=4, batch=8, C=32, S=512, B=8)
+    case = make_case(base, seed=16, name="groups")
+    d = to_device(case, gpu_device)
+    case.cfg = base.with_(batch_groups=1)
+    a = run_gpu(case, gpu_device, dev=d)
+    case.cfg = base.with_(batch_groups=8)
+    b = run_gpu(case, gpu_device, dev=d)
+    assert torch.equal(a["raw"]["spikes"], b["raw"]["spikes"])
+    assert torch.equal(_bits(a["raw"]["grads"]["grad_x"]), _bits(b["raw"]["grads"]["grad_x"]))
+    compare(case, a)
+    compare(case, b)
+
+
+def test_forward_without_checkpoints_for_inference(gpu_device):
+    import torch
+
+    c = cfg(T=12, batch=2, C=64, S=1, B=8, ckpt_every=4)
+    case = make_case(c, seed=17, name="inference")
+    d = to_device(case, gpu_device)
+    s1, v1, ck = dendsn.forward(c, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], None, want_v_soma=True)
+    s2, v2, ck2 = dendsn.forward(c, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], None, want_v_soma=True,
+                                 save_ckpt=False)
+    torch.cuda.synchronize()
+    assert ck is not None and ck2 is None
+    assert torch.equal(s1, s2) and torch.equal(v1, v2)
