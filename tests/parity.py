@@ -10,8 +10,23 @@ train), repeating until no disagreement is left; every exemption is counted and
 reported.  A disagreement outside the band fails.
 
 Tolerances.  fp32 outputs: |g - o| <= rtol (|o| + rms(o)) elementwise, rms over
-the tensor; summed parameter gradients: |g - o| <= rtol * sum|terms|.
-rtol is 1e-5 for fp32 results and 2e-2 for results stored in bf16.
+the tensor; summed parameter gradients: |g - o| <= rtol (A + rms(A)) with
+A = sum|terms| per entry and rms over the [C, B] table (a term of psi = MH can
+vanish by cancellation, (1 - u^2) near u = 1, while its rounding error does not,
+so an entry's own A alone can undercount its rounding); the scalar g_alpha:
+|g - o| <= rtol * A.
+rtol is 1e-5 for fp32 results and 2e-2 for results stored in bf16.  Every
+tensor must also meet ||g - o||_2 <= rtol ||o||_2.
+
+Long horizons.  Rounding errors of an fp32 evaluation of the leaky recurrences
+accumulate over the memory of each chain, h(x) = min(T, 1 / (1 - x)) steps for
+a decay x; the somatic potential inherits the dendrite's error (h(alpha)) and
+carries it through the soma (h(beta)), and the backward's surrogate derivative
+is steepest exactly where that potential sits.  The elementwise bounds are
+therefore scaled by g = max(1, h(beta) h(alpha) / 4), which is 1 for four-step
+layers with alpha = beta = 1/2 and 12.5 for T = 64, alpha = 0.8, beta = 0.9 (a
+plain float32 evaluation of the equations on the CPU reaches 3.0e-5 there).
+The norm-wise bound is never scaled.
 """
 
 from __future__ import annotations
@@ -168,26 +183,47 @@ def cfg_vth(case):
     return case.cfg.v_th
 
 
-def close_elementwise(name, g, o, rtol, report: Report):
+def horizon_growth(cfg, alpha: float) -> float:
+    """Elementwise tolerance factor g = max(1, h(beta) h(alpha) / 4)."""
+    h = lambda x: min(float(cfg.T), 1.0 / (1.0 - x))
+    return max(1.0, h(cfg.beta) * (h(alpha) if cfg.stateful else 1.0) / 4.0)
+
+
+def close_normwise(name, g, o, rtol, report: Report):
+    g, o = np.asarray(g, np.float64).ravel(), np.asarray(o, np.float64).ravel()
+    den = np.linalg.norm(o)
+    rel = float(np.linalg.norm(g - o) / den) if den > 0 else float(np.linalg.norm(g))
+    report.max_err[name + "|norm"] = rel
+    if not rel <= rtol:
+        raise AssertionError(f"{name}: norm-wise relative error {rel:.3e} > {rtol:g}")
+
+
+def close_elementwise(name, g, o, rtol, growth, report: Report):
+    close_normwise(name, g, o, rtol, report)
     scale = np.abs(o) + np.sqrt(np.mean(o * o)) if o.size else np.abs(o)
     err = np.abs(g - o)
     ratio = float(np.max(err / np.maximum(scale, 1e-300))) if o.size else 0.0
     report.max_err[name] = ratio
-    if not np.all(err <= rtol * scale):
-        i = np.unravel_index(np.argmax(err - rtol * scale), o.shape)
+    bound = rtol * growth * scale
+    if not np.all(err <= bound):
+        i = np.unravel_index(np.argmax(err - bound), o.shape)
         raise AssertionError(f"{name}: |gpu - oracle| too large at {i}: gpu={g[i]!r} oracle={o[i]!r} "
-                             f"(max err/scale {ratio:.3e}, rtol {rtol:g})")
+                             f"(max err/scale {ratio:.3e}, allowed {rtol * growth:.3g})")
 
 
-def close_summed(name, g, o, absum, rtol, report: Report):
+def close_summed(name, g, o, absum, rtol, growth, report: Report):
     g, o, absum = np.asarray(g, np.float64), np.asarray(o, np.float64), np.asarray(absum, np.float64)
+    if np.ndim(o):
+        close_normwise(name, g, o, rtol, report)
     err = np.abs(g - o)
-    scale = np.maximum(absum, 1e-30)
+    floor = np.sqrt(np.mean(absum * absum)) if absum.ndim else 0.0
+    scale = np.maximum(absum + floor, 1e-30)
     report.max_err[name] = float(np.max(err / scale)) if err.size else 0.0
-    if not np.all(err <= rtol * scale):
-        i = np.unravel_index(np.argmax(err - rtol * scale), np.shape(o)) if np.ndim(o) else ()
+    bound = rtol * growth * scale
+    if not np.all(err <= bound):
+        i = np.unravel_index(np.argmax(err - bound), np.shape(o)) if np.ndim(o) else ()
         raise AssertionError(f"{name}: gpu={np.asarray(g)[i]!r} oracle={np.asarray(o)[i]!r} "
-                             f"abs-sum={np.asarray(absum)[i]!r} rtol={rtol:g}")
+                             f"abs-sum={np.asarray(absum)[i]!r} allowed {rtol * growth:.3g}")
 
 
 def compare(case: Case, gpu: dict) -> Report:
@@ -197,14 +233,15 @@ def compare(case: Case, gpu: dict) -> Report:
     assert np.array_equal(gpu["S"], rec["S"])
     assert set(np.unique(gpu["S"])).issubset({0.0, 1.0})
     og = oracle_grads(case, rec)
+    gr = horizon_growth(cfg, case.alpha)
     if gpu["H"] is not None:
-        close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, rep)
+        close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, gr, rep)
     rt_io = RTOL_BF16 if cfg.io == "bf16" else RTOL_F32
-    close_elementwise("grad_x", gpu["gX"], og["gX"], rt_io, rep)
+    close_elementwise("grad_x", gpu["gX"], og["gX"], rt_io, gr, rep)
     for k in ("g_kappa", "g_xi", "g_zeta"):
-        close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, rep)
+        close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, gr, rep)
     close_summed("g_alpha", gpu["g_alpha"], og["g_alpha"] if cfg.stateful else 0.0,
-                 og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, rep)
+                 og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, gr, rep)
     if case.mask is not None:
         off = case.mask == 0
         for k in ("g_kappa", "g_xi", "g_zeta"):
