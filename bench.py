@@ -121,6 +121,8 @@ def main():
     ap.add_argument("--batch-groups", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-nbs", type=float, default=4e8, help="oracle sample size")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device copies of MIB MiB (scales the HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -129,6 +131,17 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4,
+                          "dispatches": 5}), flush=True)
+        return
 
     import paper_2412_06355_amd as dendsn
     import workloads

@@ -5,7 +5,7 @@
 
 #include <string>
 
-#include "../../include/dendsn.h"
+#include "dendsn.h"
 #include "dendsn_kernels.h"
 
 namespace dendsn {
@@ -15,8 +15,12 @@ hipError_t launch_fwd_bf16(const Plan& pl, const FwdArgs& fa, int psi, hipStream
 hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
 hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
 
+// Fixed-order float64 sums of the per-block partials into the parameter
+// gradients.  Outputs o = (c * 3 + q) * B + b, q = 0, 1, 2 for kappa, xi, zeta.
+// The last block reduces the g_alpha partials.
 __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   const int tid = threadIdx.x;
+  const int64_t nout = f.C * 3 * f.B;
   if (blockIdx.x == gridDim.x - 1) {
     __shared__ double sh[kThreads];
     double s = 0.0;
@@ -30,20 +34,27 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
     if (tid == 0 && f.ga) f.ga[0] = f.stateful ? float(sh[0]) : 0.0f;
     return;
   }
-  const int64_t o = int64_t(blockIdx.x) * kThreads + tid;
-  if (o >= f.C * f.B) return;
-  const int64_t c = o / f.B;
-  const int b = int(o % f.B);
-  const bool on = f.mask ? (f.mask[o] != 0) : true;
-  float* outs[3] = {f.gk, f.gxi, f.gz};
-  for (int q = 0; q < 3; ++q) {
-    if (!outs[q]) continue;
-    double s = 0.0;
-    for (int g = 0; g < f.G; ++g)
-      for (int j = 0; j < f.tpc; ++j)
-        s += double(f.wsP[((int64_t(g) * f.C + c) * f.tpc + j) * 3 * f.B + q * f.B + b]);
-    outs[q][o] = on ? float(s) : 0.0f;
+  int64_t o;
+  double s = 0.0;
+  if (f.wide) {  // one wave per output, lanes stride over its contiguous slots
+    o = int64_t(blockIdx.x) * (kThreads / 64) + (tid >> 6);
+    const int lane = tid & 63;
+    if (o < nout)
+      for (int64_t p = lane; p < f.P; p += 64) s += double(f.wsP[o * f.P + p]);
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (lane != 0 || o >= nout) return;
+  } else {       // one thread per output, slots in order
+    o = int64_t(blockIdx.x) * kThreads + tid;
+    if (o >= nout) return;
+    for (int64_t p = 0; p < f.P; ++p) s += double(f.wsP[p * nout + o]);
   }
+  const int64_t c = o / (3 * f.B);
+  const int q = int((o / f.B) % 3);
+  const int b = int(o % f.B);
+  float* out = q == 0 ? f.gk : (q == 1 ? f.gxi : f.gz);
+  if (!out) return;
+  const bool on = f.mask ? (f.mask[c * f.B + b] != 0) : true;
+  out[c * f.B + b] = on ? float(s) : 0.0f;
 }
 
 }  // namespace dendsn
@@ -81,6 +92,17 @@ bool choose_mapping(int B, int io, int* BL, int* L, int* fast) {
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The backward's lane split.  Any power-of-two split of a power-of-two
+// per-lane count adds the branch terms in the same pairwise tree (in-lane pairs,
+// then DPP pairs), so the backward may hold fewer branches per lane than the
+// forward (fewer stash registers, more waves) and still recompute the forward's
+// exact bits.  Generic splits (sequential in-lane sums) must match the forward.
+void bwd_mapping(int B, int io, int* BL, int* L, int* fast) {
+  choose_mapping(B, io, BL, L, fast);
+  (void)B;
+  (void)io;
+}
 
 dendsn_status check_cfg(const dendsn_cfg* c) {
   if (!c) return fail(DENDSN_E_INVALID, "cfg is NULL");
@@ -120,7 +142,10 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
 Plan make_plan(const dendsn_cfg* c, bool bwd) {
   Plan p;
   memset(&p, 0, sizeof(p));
-  choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
+  if (bwd)
+    bwd_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
+  else
+    choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
   const int L = p.L;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
@@ -135,8 +160,12 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
     p.tpc = 1; p.cpt = int32_t(p.pb / c->S);
     p.ntiles = ceil_div(c->C, p.cpt);
   }
+  // Batch groups (measured on MI355X): the backward wants ~16K waves in the grid
+  // (more groups mean more partial sums to reduce); the forward over conv
+  // layers does best with about four batch items per lane.
   const int64_t target_waves = 16384;
   int64_t G = ceil_div(target_waves, p.ntiles * 4);
+  if (!bwd && p.mode == kSpatial) G = ceil_div(c->batch, 4);
   G = G < 1 ? 1 : G;
   const int64_t max_g = ceil_div(c->batch, p.ways);
   if (G > max_g) G = max_g;
@@ -156,14 +185,18 @@ size_t ckpt_bytes(const dendsn_cfg* c, const Plan& p) {
 }
 
 void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) {
-  const size_t nP = size_t(p.G) * size_t(c->C) * size_t(p.tpc) * 3 * size_t(c->B);
+  const size_t nP = size_t(p.G) * size_t(p.tpc) * size_t(c->C) * 3 * size_t(c->B);
   const size_t nA = size_t(p.G) * size_t(p.ntiles);
   *offA = ((nP * sizeof(float) + 255) / 256) * 256;
   *total = *offA + nA * sizeof(float);
 }
 
-dendsn_status check_grid(const Plan& p) {
+dendsn_status check_grid(const dendsn_cfg* c, const Plan& p) {
   if (p.ntiles * p.G > int64_t(INT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "grid too large");
+  if (c->C * 3 * c->B / (kThreads / 64) + 2 > int64_t(INT32_MAX))
+    return fail(DENDSN_E_UNSUPPORTED, "too many parameter-gradient outputs");
+  // per-lane byte offsets inside one sample's slice are 32-bit
+  if (c->C * c->S * c->B * 4 > int64_t(UINT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "sample slice above 4 GiB");
   return DENDSN_OK;
 }
 
@@ -237,7 +270,7 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
       (zeta && !aligned(zeta, 4)) || (v_soma && !aligned(v_soma, 4)))
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
   const Plan p = make_plan(cfg, false);
-  if ((st = check_grid(p)) != DENDSN_OK) return st;
+  if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
   FwdArgs fa;
   memset(&fa, 0, sizeof(fa));
   fill_scan(cfg, p, x, alpha, kappa, xi, zeta, mask, &fa.s);
@@ -280,7 +313,7 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   if (!aligned(workspace, 16)) return fail(DENDSN_E_WORKSPACE, "workspace must be 16-byte aligned");
   if (workspace_bytes < total)
     return fail(DENDSN_E_WORKSPACE, "workspace smaller than dendsn_bwd_workspace_bytes()");
-  if ((st = check_grid(p)) != DENDSN_OK) return st;
+  if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
 
   BwdArgs ba;
   memset(&ba, 0, sizeof(ba));
@@ -291,6 +324,8 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   ba.gx = grad_x;
   ba.wsP = static_cast<float*>(workspace);
   ba.wsA = reinterpret_cast<float*>(static_cast<char*>(workspace) + offA);
+  ba.P = int64_t(p.G) * p.tpc;
+  ba.wide = ba.P > kNarrowSlots;
   ba.detach = cfg->detach_reset;
   ba.sg = cfg->sg;
   ba.sg_scale = cfg->sg_scale;
@@ -302,9 +337,10 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   memset(&f, 0, sizeof(f));
   f.wsP = ba.wsP; f.wsA = ba.wsA; f.mask = mask;
   f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha;
-  f.C = cfg->C; f.B = cfg->B; f.G = p.G; f.tpc = p.tpc; f.stateful = cfg->stateful;
+  f.C = cfg->C; f.B = cfg->B; f.P = ba.P; f.wide = ba.wide; f.stateful = cfg->stateful;
   f.nA = int64_t(p.G) * p.ntiles;
-  const int64_t nblk = ceil_div(cfg->C * cfg->B, kThreads) + 1;
+  const int64_t nout = cfg->C * 3 * cfg->B;
+  const int64_t nblk = (f.wide ? ceil_div(nout, kThreads / 64) : ceil_div(nout, kThreads)) + 1;
   dendsn_finalize_kernel<<<dim3(unsigned(nblk)), dim3(kThreads), 0, stream>>>(f);
   e = hipGetLastError();
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("finalize launch: ") + hipGetErrorString(e));

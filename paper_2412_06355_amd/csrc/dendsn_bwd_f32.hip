@@ -25,6 +25,7 @@ hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int psi, hipStream_
   if (pl.BL == BL_ && pl.L == L_ && !pl.fast && pl.KS == DENDSN_GENERIC_KS)         \
     return launch_bwd_ks<BL_, L_, DENDSN_GENERIC_KS>(grid, ba, psi, stream);
   DENDSN_FAST_F32(DENDSN_FAST_CASE)
+  DENDSN_BWD_HALF(DENDSN_FAST_CASE)
   DENDSN_GENERIC(DENDSN_GENERIC_CASE)
 #undef DENDSN_FAST_CASE
 #undef DENDSN_GENERIC_CASE

@@ -48,23 +48,30 @@ __device__ __forceinline__ bf16_t to_bf16(float a) {
   return __builtin_bit_cast(bf16_t, static_cast<__bf16>(a));
 }
 
+// Streaming loads are non-temporal: X, grad_spikes and checkpoints are read
+// once per pass, so they should not displace anything in the caches.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
 template <int BL>
 __device__ __forceinline__ void load_vec(const float* __restrict__ p, float (&v)[BL]) {
   if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
-      const float4 q = reinterpret_cast<const float4*>(p)[i];
+      const f32x4_t q = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p) + i);
       v[4 * i] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
     }
   } else if constexpr (BL % 2 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 2; ++i) {
-      const float2 q = reinterpret_cast<const float2*>(p)[i];
+      const f32x2_t q = __builtin_nontemporal_load(reinterpret_cast<const f32x2_t*>(p) + i);
       v[2 * i] = q.x; v[2 * i + 1] = q.y;
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < BL; ++i) v[i] = p[i];
+    for (int i = 0; i < BL; ++i) v[i] = __builtin_nontemporal_load(p + i);
   }
 }
 
@@ -73,7 +80,7 @@ __device__ __forceinline__ void load_vec(const bf16_t* __restrict__ p, float (&v
   if constexpr (BL % 8 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 8; ++i) {
-      const uint4 q = reinterpret_cast<const uint4*>(p)[i];
+      const u32x4_t q = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p) + i);
       v[8 * i + 0] = bf16_lo(q.x); v[8 * i + 1] = bf16_hi(q.x);
       v[8 * i + 2] = bf16_lo(q.y); v[8 * i + 3] = bf16_hi(q.y);
       v[8 * i + 4] = bf16_lo(q.z); v[8 * i + 5] = bf16_hi(q.z);
@@ -82,19 +89,19 @@ __device__ __forceinline__ void load_vec(const bf16_t* __restrict__ p, float (&v
   } else if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
-      const uint2 q = reinterpret_cast<const uint2*>(p)[i];
+      const u32x2_t q = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p) + i);
       v[4 * i + 0] = bf16_lo(q.x); v[4 * i + 1] = bf16_hi(q.x);
       v[4 * i + 2] = bf16_lo(q.y); v[4 * i + 3] = bf16_hi(q.y);
     }
   } else if constexpr (BL % 2 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 2; ++i) {
-      const uint32_t q = reinterpret_cast<const uint32_t*>(p)[i];
+      const uint32_t q = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + i);
       v[2 * i] = bf16_lo(q); v[2 * i + 1] = bf16_hi(q);
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < BL; ++i) v[i] = bf16_lo(p[i]);
+    for (int i = 0; i < BL; ++i) v[i] = bf16_lo(__builtin_nontemporal_load(p + i));
   }
 }
 
@@ -152,8 +159,54 @@ __device__ __forceinline__ const P* at(const P* base, uint32_t off) {
   return reinterpret_cast<const P*>(reinterpret_cast<const char*>(base) + off);
 }
 
-__device__ __forceinline__ float load_one(const float* p) { return *p; }
-__device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(*p); }
+// grad_x is written once and never read back by the kernels: non-temporal stores.
+template <int BL>
+__device__ __forceinline__ void store_vec_nt(float* __restrict__ p, const float (&v)[BL]) {
+  if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const f32x4_t q = {v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+      __builtin_nontemporal_store(q, reinterpret_cast<f32x4_t*>(p) + i);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const f32x2_t q = {v[2 * i], v[2 * i + 1]};
+      __builtin_nontemporal_store(q, reinterpret_cast<f32x2_t*>(p) + i);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) __builtin_nontemporal_store(v[i], p + i);
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void store_vec_nt(bf16_t* __restrict__ p, const float (&v)[BL]) {
+  if constexpr (BL % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 8; ++i) {
+      const u32x4_t q = {pack_bf16x2(v[8 * i + 0], v[8 * i + 1]), pack_bf16x2(v[8 * i + 2], v[8 * i + 3]),
+                         pack_bf16x2(v[8 * i + 4], v[8 * i + 5]), pack_bf16x2(v[8 * i + 6], v[8 * i + 7])};
+      __builtin_nontemporal_store(q, reinterpret_cast<u32x4_t*>(p) + i);
+    }
+  } else if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const u32x2_t q = {pack_bf16x2(v[4 * i + 0], v[4 * i + 1]), pack_bf16x2(v[4 * i + 2], v[4 * i + 3])};
+      __builtin_nontemporal_store(q, reinterpret_cast<u32x2_t*>(p) + i);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i)
+      __builtin_nontemporal_store(pack_bf16x2(v[2 * i], v[2 * i + 1]), reinterpret_cast<uint32_t*>(p) + i);
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) __builtin_nontemporal_store(to_bf16(v[i]), p + i);
+  }
+}
+
+__device__ __forceinline__ float load_one(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__builtin_nontemporal_load(p)); }
 __device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
 __device__ __forceinline__ void store_spike(bf16_t* p, bool s) { *p = s ? bf16_t(0x3f80) : bf16_t(0); }
 
@@ -363,48 +416,68 @@ __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, 
   }
 }
 
-template <typename IO, int BL, int L, int PSI, int D>
+// Running state of the neuron a lane is computing, and wave-uniform output
+// pointers of its batch item (advanced step by step, never recomputed).
+template <typename IO, int BL>
 struct FwdLane {
-  // running state of the neuron being computed
   float vd[BL];
   float h;
   bool s;
-  int t;          // step index of the chunk being computed
-  int64_t n0;     // first neuron of the current batch item (uniform)
+  int t;          // step index of the chunk being computed (0 .. Tp-1)
+  int kc;         // steps until the next checkpoint
+  IO* sp;         // spikes row t of this batch item
+  float* vp;      // v_soma row t (or null)
+  float* ckv;     // next checkpoint's dendritic-state block of this item
+  float* ckh;     // next checkpoint's H row of this item
 };
+
+template <typename IO, int BL>
+__device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, FwdLane<IO, BL>& st) {
+  const ScanArgs& a = fa.s;
+  st.t = 0;
+  st.kc = a.K;
+  st.sp = static_cast<IO*>(fa.spikes) + n0;
+  st.vp = fa.vsoma ? fa.vsoma + n0 : nullptr;
+  st.ckv = fa.ckpt ? fa.ckpt + n0 * a.B : nullptr;
+  st.ckh = fa.ckpt ? fa.ckpt + int64_t(a.nck) * a.N * a.B + n0 : nullptr;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) st.vd[j] = 0.0f;
+  st.h = 0.0f;
+  st.s = false;
+}
 
 template <typename IO, int BL, int L, int PSI, int D>
 __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL>& br,
                                               float alpha, bool lead, int T, int Tp, int64_t item_neurons,
-                                              const float (&buf)[D][BL], FwdLane<IO, BL, L, PSI, D>& st) {
+                                              const float (&buf)[D][BL], FwdLane<IO, BL>& st) {
   const ScanArgs& a = fa.s;
-  const bool fresh = st.t == 0;
-#pragma unroll
-  for (int j = 0; j < BL; ++j) st.vd[j] = fresh ? 0.0f : st.vd[j];
-  st.h = fresh ? 0.0f : st.h;
-  st.s = fresh ? false : st.s;
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = st.t + k;
     const float z = dendrite_step<BL, L, PSI>(st.vd, buf[k], br, alpha);
     soma_step(st.h, st.s, z, a.beta, a.vth);
-    if (t < T) {
-      const int64_t row = int64_t(t) * a.N + st.n0;
+    if (t < T) {  // padded steps store nothing
       if (lead) {
-        store_spike(at(static_cast<IO*>(fa.spikes) + row, lo.s), st.s);
-        if (fa.vsoma) *at(fa.vsoma + row, lo.v) = st.h;
+        store_spike(at(st.sp, lo.s), st.s);
+        if (st.vp) *at(st.vp, lo.v) = st.h;
       }
-      if (fa.ckpt && (t + 1) % a.K == 0 && t + 1 < T) {
-        const int64_t kk = (t + 1) / a.K - 1;
-        store_vec<BL>(at(fa.ckpt + (kk * a.N + st.n0) * a.B, lo.c), st.vd);
-        if (lead) *at(fa.ckpt + int64_t(a.nck) * a.N * a.B + kk * a.N + st.n0, lo.v) = st.h;
+      if (--st.kc == 0) {
+        st.kc = a.K;
+        if (st.ckv && t + 1 < T) {
+          store_vec<BL>(at(st.ckv, lo.c), st.vd);
+          if (lead) *at(st.ckh, lo.v) = st.h;
+          st.ckv += a.N * a.B;
+          st.ckh += a.N;
+        }
       }
+      st.sp += a.N;
+      if (st.vp) st.vp += a.N;
     }
   }
   st.t += D;
-  if (st.t >= Tp) {
-    st.t = 0;
-    st.n0 += item_neurons;
+  if (st.t >= Tp) {  // next batch item of this lane
+    const int64_t n0 = (st.sp - static_cast<IO*>(fa.spikes)) - int64_t(T) * a.N + item_neurons;
+    fwd_item_start<IO, BL>(fa, n0, st);
   }
 }
 
@@ -431,13 +504,8 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   cur.base = static_cast<const IO*>(a.x) + bt0 * a.M * a.B;
   cur.k = 0;
   cur.t = 0;
-  FwdLane<IO, BL, L, PSI, D> st;
-  st.t = 0;
-  st.n0 = bt0 * a.M;
-#pragma unroll
-  for (int j = 0; j < BL; ++j) st.vd[j] = 0.0f;
-  st.h = 0.0f;
-  st.s = false;
+  FwdLane<IO, BL> st;
+  fwd_item_start<IO, BL>(fa, bt0 * a.M, st);
 
   float bufA[D][BL], bufB[D][BL];
   if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
@@ -474,58 +542,118 @@ struct BwdLane {  // adjoint state carried backwards through time, and pointers
   const float* gvbase;
 };
 
-template <typename IO, int BL, int L, int PSI, int CS>
-__device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
-                                          float alpha, float beta_r, int c0, const float (&v0)[BL], float h0,
-                                          bool s0, BwdLane<IO, BL>& bl, Accum<BL>& acc) {
-  const ScanArgs& a = ba.s;
+// The streamed inputs of one chunk of CS steps.
+template <int BL, int CS>
+struct ChunkIn {
+  float x[CS][BL];
+  float gs[CS];
+  float gv[CS];
+};
+
+// grad_v_soma rows of a chunk (0 without grad_v_soma); issued with the chunk's
+// other loads so no step waits on a load issued after its stores.
+template <int BL, int CS>
+__device__ __forceinline__ void load_chunk_gv(const ScanArgs& a, const LaneOff& lo, const float* gvbase, int c0,
+                                              ChunkIn<BL, CS>& in) {
+  if (gvbase) {
+#pragma unroll
+    for (int k = 0; k < CS; ++k) in.gv[k] = __builtin_nontemporal_load(at(gvbase + int64_t(c0 + k) * a.N, lo.v));
+  } else {
+#pragma unroll
+    for (int k = 0; k < CS; ++k) in.gv[k] = 0.0f;
+  }
+}
+
+template <typename IO, int BL, int CS>
+__device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
+                                              const IO* gsbase, const float* gvbase, int c0, ChunkIn<BL, CS>& in) {
   const int64_t rowX = a.N * a.B;
-  const float beta = a.beta, vth = a.vth;
-  float xb[CS][BL];
-  float gsb[CS];
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
     const int64_t t = c0 + k;
-    load_vec<BL>(at(bl.xbase + t * rowX, lo.x), xb[k]);
-    gsb[k] = load_one(at(bl.gsbase + t * a.N, lo.s));
+    load_vec<BL>(at(xbase + t * rowX, lo.x), in.x[k]);
+    in.gs[k] = load_one(at(gsbase + t * a.N, lo.s));
   }
-  // Recompute the chunk's steps exactly as the forward did (same inline step
-  // function); stash Vd, H and, for the Mexican hat, its exp(-u^2/2) factor.
-  float stv[CS + 1][BL];
-  float ste[PSI == 1 ? CS : 1][BL];
-  float sth[CS];
+  load_chunk_gv<BL, CS>(a, lo, gvbase, c0, in);
+}
+
+// The checkpointed state a segment starts from.
+template <int BL>
+struct SegStart {
+  float v[BL];
+  float h;
+};
+
+template <typename IO, int BL>
+__device__ __forceinline__ void load_seg_start(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int seg,
+                                               SegStart<BL>& st) {
+  const ScanArgs& a = ba.s;
+  if (seg == 0) {
 #pragma unroll
-  for (int j = 0; j < BL; ++j) stv[0][j] = v0[j];
-  {
-    float h = h0;
-    bool s = s0;
-#pragma unroll
-    for (int k = 0; k < CS; ++k) {
-#pragma unroll
-      for (int j = 0; j < BL; ++j) stv[k + 1][j] = stv[k][j];
-      const float z = dendrite_step<BL, L, PSI>(stv[k + 1], xb[k], br, alpha, PSI == 1 ? ste[PSI == 1 ? k : 0] : nullptr);
-      soma_step(h, s, z, beta, vth);
-      sth[k] = h;
-    }
+    for (int j = 0; j < BL; ++j) st.v[j] = 0.0f;
+    st.h = 0.0f;
+  } else {
+    load_vec<BL>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.B, lo.c), st.v);
+    st.h = __builtin_nontemporal_load(at(ba.ckpt + int64_t(a.nck) * a.N * a.B + int64_t(seg - 1) * a.N + n0, lo.v));
   }
-  // Adjoint recurrences, last step first.
+}
+
+// Registers a chunk's recompute leaves for its adjoint pass: the dendritic
+// state before and at each step, H at each step and, for the Mexican hat, the
+// exp(-u^2/2) factor of each step.
+template <int BL, int CS, int PSI>
+struct Stash {
+  float v[CS + 1][BL];
+  float e[PSI == 1 ? CS : 1][BL];
+  float h[CS];
+};
+
+// Re-runs the chunk's forward steps exactly as the forward kernel did (the same
+// inline step function, so the same bits).
+template <int BL, int L, int PSI, int CS>
+__device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branches<BL>& br, float alpha,
+                                                const float (&v0)[BL], float h0, bool s0,
+                                                const float (&x)[CS][BL], Stash<BL, CS, PSI>& st) {
+#pragma unroll
+  for (int j = 0; j < BL; ++j) st.v[0][j] = v0[j];
+  float h = h0;
+  bool s = s0;
+#pragma unroll
+  for (int k = 0; k < CS; ++k) {
+#pragma unroll
+    for (int j = 0; j < BL; ++j) st.v[k + 1][j] = st.v[k][j];
+    const float z = dendrite_step<BL, L, PSI>(st.v[k + 1], x[k], br, alpha, PSI == 1 ? st.e[PSI == 1 ? k : 0] : nullptr);
+    soma_step(h, s, z, a.beta, a.vth);
+    st.h[k] = h;
+  }
+}
+
+// The adjoint recurrences through one chunk, last step first; writes grad_x
+// and accumulates the parameter gradients.
+template <typename IO, int BL, int L, int PSI, int CS>
+__device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+                                              float alpha, float beta_r, int c0, const Stash<BL, CS, PSI>& st,
+                                              const float (&gs)[CS], const float (&gvr)[CS], BwdLane<IO, BL>& bl,
+                                              Accum<BL>& acc) {
+  const ScanArgs& a = ba.s;
+  const int64_t rowX = a.N * a.B;
+  const float beta = a.beta, vth = a.vth;
 #pragma unroll
   for (int k = CS - 1; k >= 0; --k) {
-    const float hk = sth[k];
+    const float hk = st.h[k];
     const bool sk = hk >= vth;
-    const float gv = bl.gvbase ? *at(bl.gvbase + int64_t(c0 + k) * a.N, lo.v) : 0.0f;
     const float sgv = surrogate(hk - vth, ba.sg, ba.sg_scale);
-    const float dS = fmaf(-beta_r * hk, bl.dh_next, gsb[k]);  // beta_r = 0: reset detached
-    float dh = fmaf(sgv, dS, gv);
+    const float dS = fmaf(-beta_r * hk, bl.dh_next, gs[k]);  // beta_r = 0: reset detached
+    float dh = fmaf(sgv, dS, gvr[k]);
     dh = sk ? dh : fmaf(beta, bl.dh_next, dh);
     float gxo[BL];
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
-      const float tt = (stv[k + 1][j] - br.xi[j]) * br.rz[j];
+      const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
       float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
       if constexpr (PSI == 1) {
         const float q = tt * tt;
-        const float e = ste[PSI == 1 ? k : 0][j];
+        const float e = st.e[PSI == 1 ? k : 0][j];
         y = (1.0f - q) * e;
         dps = tt * (q - 3.0f) * e;
       } else {
@@ -538,11 +666,21 @@ __device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, 
       acc.k[j] = fmaf(dh, y, acc.k[j]);
       acc.xi[j] -= r;
       acc.z[j] = fmaf(-r, tt, acc.z[j]);
-      acc.a = fmaf(bl.lam[j], stv[k][j], acc.a);
+      acc.a = fmaf(bl.lam[j], st.v[k][j], acc.a);
     }
-    store_vec<BL>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
+    store_vec_nt<BL>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
     bl.dh_next = dh;
   }
+}
+
+template <typename IO, int BL, int L, int PSI, int CS>
+__device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+                                          float alpha, float beta_r, int c0, const float (&v0)[BL], float h0,
+                                          bool s0, const ChunkIn<BL, CS>& in, BwdLane<IO, BL>& bl,
+                                          Accum<BL>& acc) {
+  Stash<BL, CS, PSI> st;
+  recompute_chunk<BL, L, PSI, CS>(ba.s, br, alpha, v0, h0, s0, in.x, st);
+  reverse_chunk<IO, BL, L, PSI, CS>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
 }
 
 // Runs the forward from (vd, h, s) at step t_from up to (not including) t_to.
@@ -559,13 +697,33 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
   }
 }
 
+// Loads a chunk of CS steps and runs it (used for every chunk but a prefetched one).
+template <typename IO, int BL, int L, int PSI, int CS>
+__device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+                                                   float alpha, float beta_r, int t0, int c0, const SegStart<BL>& ss,
+                                                   BwdLane<IO, BL>& bl, Accum<BL>& acc) {
+  ChunkIn<BL, CS> in;
+  load_chunk_in<IO, BL, CS>(ba.s, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+  float v[BL];
+#pragma unroll
+  for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
+  float h = ss.h;
+  bool s = ss.h >= ba.s.vth && t0 > 0;
+  advance<IO, BL, L, PSI>(ba.s, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+  bwd_chunk<IO, BL, L, PSI, CS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+}
+
+// Chunk plan of a segment [t0, t1): whole KS-step chunks from t0, then the
+// remainder in descending powers of two, placed from the top down; visited
+// from the last step backwards.  A neuron's first visited chunk is the top of
+// its last segment; it is a full KS chunk exactly when that segment's length
+// is a multiple of KS, and only then is it prefetched.
 template <typename IO, int BL, int L, int PSI, int KS>
 __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff& lo, int64_t bt,
                                                 const Branches<BL>& br, float alpha, Accum<BL>& acc) {
   const ScanArgs& a = ba.s;
   const int T = int(a.T);
   const int K = a.K;
-  const float vth = a.vth;
   const float beta_r = ba.detach ? 0.0f : a.beta;
   const int64_t n0 = bt * a.M;  // first neuron of this batch item (wave-uniform)
   BwdLane<IO, BL> bl;
@@ -581,54 +739,88 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
   for (int seg = nseg - 1; seg >= 0; --seg) {
     const int t0 = seg * K;
     const int t1 = min(T, t0 + K);
-    float vs[BL];
-    float hs = 0.0f;
-    if (seg == 0) {
-#pragma unroll
-      for (int j = 0; j < BL; ++j) vs[j] = 0.0f;
-    } else {
-      load_vec<BL>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.B, lo.c), vs);
-      hs = *at(ba.ckpt + int64_t(a.nck) * a.N * a.B + int64_t(seg - 1) * a.N + n0, lo.v);
-    }
-    const bool ss = (seg > 0) && (hs >= vth);
-    // Chunks: full KS-step chunks from t0, then the remainder in descending
-    // powers of two; visited from the last one back to t0.
+    SegStart<BL> ss;
+    load_seg_start<IO, BL>(ba, lo, n0, seg, ss);
+    // Chunks: the remainder (len mod KS) first, in descending powers of two
+    // from t0, then whole KS-step chunks; visited from the last one back.  A
+    // chunk re-runs the forward from t0 up to its first step, so putting the
+    // short pieces first keeps that re-advance as short as possible.
     const int len = t1 - t0;
     const int nfull = len / KS;
     const int rem = len - nfull * KS;
-    int end = t1;
+    for (int ch = nfull - 1; ch >= 0; --ch) {
+      const int c0 = t0 + rem + ch * KS;
+      ChunkIn<BL, KS> in;
+      load_chunk_in<IO, BL, KS>(a, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+      float v[BL];
+#pragma unroll
+      for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
+      float h = ss.h;
+      bool s = ss.h >= a.vth && t0 > 0;
+      advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+      bwd_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+    }
+    // remainder pieces fill [t0, t0 + rem) with the largest on top and the
+    // smallest at t0 (their re-advances then sum to the least); top one first
+    int top = t0 + rem;
 #pragma unroll
     for (int cs = KS / 2; cs >= 1; cs /= 2) {
       if (rem & cs) {
-        // This piece is the highest-placed remainder chunk not yet visited: it
-        // sits just below `end`.
-        const int c0 = end - cs;
-        float v[BL];
-#pragma unroll
-        for (int j = 0; j < BL; ++j) v[j] = vs[j];
-        float h = hs;
-        bool s = ss;
-        advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-        if constexpr (KS / 2 >= 1) {
-          if (cs == 8) bwd_chunk<IO, BL, L, PSI, (KS >= 16 ? 8 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
-          else if (cs == 4) bwd_chunk<IO, BL, L, PSI, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
-          else if (cs == 2) bwd_chunk<IO, BL, L, PSI, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
-          else bwd_chunk<IO, BL, L, PSI, 1>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
-        }
-        end = c0;
+        const int c0 = top - cs;
+        if (cs == 4) load_and_run_chunk<IO, BL, L, PSI, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else if (cs == 2) load_and_run_chunk<IO, BL, L, PSI, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else load_and_run_chunk<IO, BL, L, PSI, 1>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        top = c0;
       }
     }
-    for (int ch = nfull - 1; ch >= 0; --ch) {
-      const int c0 = t0 + ch * KS;
-      float v[BL];
-#pragma unroll
-      for (int j = 0; j < BL; ++j) v[j] = vs[j];
-      float h = hs;
-      bool s = ss;
-      advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-      bwd_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, bl, acc);
-    }
   }
+}
+
+// The common short-sequence case: T == KS, so every neuron is one chunk that
+// starts from the zero state.  Software-pipelined over the lane's neurons: the
+// next neuron's rows are requested right after this neuron's recompute, when
+// the registers of its own rows are free again, so they stream in while the
+// adjoint pass runs.
+template <typename IO, int BL, int L, int PSI, int KS>
+__device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+                                                   float alpha, int64_t bt0, int nk, Accum<BL>& acc) {
+  const ScanArgs& a = ba.s;
+  const float beta_r = ba.detach ? 0.0f : a.beta;
+  const int64_t step = int64_t(a.ways) * a.M;  // neurons between this lane's items
+  int64_t n0 = bt0 * a.M;
+  const IO* x = static_cast<const IO*>(a.x);
+  const IO* g = static_cast<const IO*>(ba.gspk);
+  ChunkIn<BL, KS> cur;
+  if (nk > 0) load_chunk_in<IO, BL, KS>(a, lo, x + n0 * a.B, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
+  float zero[BL];
+#pragma unroll
+  for (int j = 0; j < BL; ++j) zero[j] = 0.0f;
+  for (int i = 0; i < nk; ++i) {
+    BwdLane<IO, BL> bl;
+    bl.xbase = x + n0 * a.B;
+    bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.B;
+    bl.gsbase = g + n0;
+    bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
+    bl.dh_next = 0.0f;
+#pragma unroll
+    for (int j = 0; j < BL; ++j) bl.lam[j] = 0.0f;
+    Stash<BL, KS, PSI> st;
+    recompute_chunk<BL, L, PSI, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
+    ChunkIn<BL, KS> nxt;
+    const int64_t n1 = n0 + step;
+    if (i + 1 < nk) load_chunk_in<IO, BL, KS>(a, lo, x + n1 * a.B, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
+    reverse_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
+    cur = nxt;
+    n0 = n1;
+  }
+}
+
+// Where partial slot p of output (c, q, b) lives in the workspace: output-major
+// ([3CB][P], read by one wave per output) when there are many slots, slot-major
+// ([P][3CB], read by one thread per output) when there are few.
+__device__ __forceinline__ int64_t partial_index(const BwdArgs& ba, int64_t c, int q, int b, int64_t p) {
+  const int64_t o = (c * 3 + q) * ba.s.B + b;
+  return ba.wide ? o * ba.P + p : p * (3 * ba.s.C * ba.s.B) + o;
 }
 
 // Block reduction of the parameter-gradient partials, in a fixed order.
@@ -666,7 +858,7 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
       const int sub = b / BL, j = b % BL;
       float s = 0.0f;
       for (int w = 0; w < 4; ++w) s += red[((q * BL + j) * 4 + w) * L + sub];
-      ba.wsP[((int64_t(pos.g) * a.C + c) * a.tpc + jt) * 3 * B + q * B + b] = s;
+      ba.wsP[partial_index(ba, c, q, b, int64_t(pos.g) * a.tpc + jt)] = s;
     }
   } else {
     // Whole channels per tile: sum the batch ways and the S positions of each channel.
@@ -686,7 +878,7 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
             const int thr = (w * a.pb + slot * int(a.S) + sp) * L + sub;
             s += red[thr * BL + j];
           }
-        ba.wsP[(int64_t(pos.g) * a.C + c) * 3 * B + q * B + b] = s;
+        ba.wsP[partial_index(ba, c, q, b, pos.g)] = s;
       }
       __syncthreads();
     }
@@ -696,7 +888,7 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
 }
 
 template <typename IO, int BL, int L, int PSI, int KS>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * KS <= 16 ? 3 : 2))) dendsn_bwd_kernel(BwdArgs ba) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * KS <= 8 ? 4 : (BL * KS <= 16 ? 3 : 2)))) dendsn_bwd_kernel(BwdArgs ba) {
   const ScanArgs& a = ba.s;
   const Pos pos = locate<L>(a);
   Accum<BL> acc;
@@ -710,8 +902,20 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     const LaneOff lo = lane_offsets<IO, BL>(a, pos);
     int64_t bt0;
     const int nk = items_of(a, pos, &bt0);
-    for (int i = 0; i < nk; ++i) backward_neuron<IO, BL, L, PSI, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
+    const int T = int(a.T);
+    bool single = false;
+    if constexpr (KS == 4) {
+      if (T == KS) {
+        single_chunk_items<IO, BL, L, PSI, KS>(ba, lo, br, alpha, bt0, nk, acc);
+        single = true;
+      }
+    }
+    if (!single) {
+      for (int i = 0; i < nk; ++i)
+        backward_neuron<IO, BL, L, PSI, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
+    }
   }
+  // every thread of the block reaches this one call (it holds block barriers)
   reduce_partials<BL, L>(ba, pos, acc);
 }
 

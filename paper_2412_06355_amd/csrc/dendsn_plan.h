@@ -60,8 +60,10 @@ struct BwdArgs {
   const void* gspk;
   const float* gv;  // optional
   void* gx;
-  float* wsP;       // [G][C][tpc][3][B] partial sums of (g_kappa, g_xi, g_zeta)
+  float* wsP;       // partial sums of (g_kappa, g_xi, g_zeta): P slots per output, see partial_index
   float* wsA;       // [G][ntiles] partial sums of g_alpha
+  int64_t P;        // partial slots per output: G * tpc
+  int32_t wide;     // 1: output-major layout (P > kNarrowSlots)
   int32_t detach;
   int32_t sg;
   float sg_scale;
@@ -75,15 +77,20 @@ struct FinArgs {
   float* gxi;
   float* gz;
   float* ga;
-  int64_t C, nA;
-  int32_t B, G, tpc, stateful;
+  int64_t C, nA, P;
+  int32_t B, wide, stateful;
 };
+
+constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread per output
 
 // Compiled (BL, L) mappings.  "Fast" mappings move 8 or 16 bytes per lane;
 // "generic" ones cover other branch counts.  Backward stash capacities: 4 steps
 // for every mapping, and 8 steps too when a lane holds at most 4 branches.
 #define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
 #define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
+// Backward-only splits with 2 branches per lane (same branch-sum tree as the
+// forward's 4 or 8 per lane, so the recompute stays bit-identical).
+#define DENDSN_BWD_HALF(X) X(2, 2) X(2, 4) X(2, 8) X(2, 16)
 #define DENDSN_GENERIC(X) X(1, 1) X(2, 1) X(3, 1) X(5, 1) X(6, 1) X(7, 1) X(5, 2) X(6, 2) X(7, 2)
 #define DENDSN_GENERIC_KS 4
 
