@@ -20,6 +20,7 @@ Forward recurrences, in the paper's order (Methods, "Dendritic spiking neuron"):
                                     Y_b[t]  = psi(u_b[t])
   Eq. (methods-mexican-hat)         psi(x)  = (1 - x^2) exp(-x^2 / 2)   ("MH"), or psi(x) = x ("Identity")
   Eq. (methods-soma-input)          Z[t]    = sum_b kappa*_b Y_b[t]
+  Eq. (methods-residual)            Z[t]   += (1/P) sum_i X_i[t]   (ResStateful / ResStateless variants)
   Eq. (methods-dbg-mask)            kappa*  = kappa (.) m   (dendritic branch gating; m = 1 without a mask)
   Eq. (methods-lif-reset-charge)    H[t]    = beta (1 - S[t-1]) H[t-1] + Z[t],  H[0] = 0, S[0] = 0
   Eq. (methods-lif-fire)            S[t]    = Theta(H[t] - v_th),  Theta(x) = 1 iff x >= 0
@@ -35,10 +36,12 @@ are the chain rule applied to the forward recurrences above, in reverse time:
 
   dS[t]   = gS[t] - beta H[t] dH[t+1]                 (second term dropped when the reset is detached)
   dH[t]   = gV[t] + sg(H[t] - v_th) dS[t] + beta (1 - S[t]) dH[t+1]
+  g_beta += dH[t] (1 - S[t-1]) H[t-1]                 (PLIF soma: beta learnable)
   g_u     = kappa*_b dH[t] psi'(u_b[t])
   r_b[t]  = g_u sgn(Vd_b[t] - xi_b) / zeta_b          (sgn(0) = 0: the L2 norm's subgradient at 0)
   lam_b[t]= r_b[t] + alpha lam_b[t+1]                 (Stateless: lam = r)
-  gX      = lam;   g_kappa += m dH Y;  g_xi += -r;  g_zeta += -g_u u / zeta;  g_alpha += lam_b[t] Vd_b[t-1]
+  gX      = lam (+ dH / P with the residual term);
+  g_kappa += m dH Y;  g_xi += -r;  g_zeta += -g_u u / zeta;  g_alpha += lam_b[t] Vd_b[t-1]
 
 The backward consumes the recorded spikes S rather than re-deciding Theta, so
 that the oracle's gradient is exactly the gradient of the forward whose spikes
@@ -151,6 +154,7 @@ def forward(
     S: int = 1,
     psi_kind: str = PSI_MEXHAT,
     stateful: bool = True,
+    residual: bool = False,
     force: np.ndarray | None = None,
 ) -> dict:
     """Run the DendSN layer forward over all T steps.
@@ -200,6 +204,10 @@ def forward(
         # Eq. (methods-soma-input) with the gated strengths of Eq. (methods-dbg-mask).
         # A gated-off branch contributes nothing, whatever its Y.
         Z[t] = np.where(m_n != 0, kstar_n * Y[t], 0.0).sum(axis=1)
+        if residual:
+            # Eq. (methods-residual): the mean synaptic input of the P compartments
+            # (gating scales branch strengths only, so every compartment takes part).
+            Z[t] = Z[t] + X[t].mean(axis=1)
         # Eq. (methods-lif-reset-charge) and Eq. (methods-lif-fire).
         H[t] = beta * (1.0 - s_prev) * h_prev + Z[t]
         s = (H[t] - v_th >= 0.0).astype(np.float64)
@@ -213,7 +221,7 @@ def forward(
         X=X, Vd=Vd, d=d, u=u, Y=Y, Z=Z, H=H, S=Sp,
         alpha=float(alpha), beta=float(beta), v_th=float(v_th),
         kappa=kappa, xi=xi, zeta=zeta, m=m, C=C, S_sp=S, batch=batch,
-        psi_kind=psi_kind, stateful=bool(stateful),
+        psi_kind=psi_kind, stateful=bool(stateful), residual=bool(residual),
     )
 
 
@@ -249,6 +257,7 @@ def backward(
 
     dH = np.zeros((T, N))
     gX = np.zeros((T, N, B))
+    t_beta = np.zeros((T, N))
     t_kappa = np.zeros((T, N, B))
     t_xi = np.zeros((T, N, B))
     t_zeta = np.zeros((T, N, B))
@@ -265,7 +274,10 @@ def backward(
         g_u = kstar_n * dH[t][:, None] * dpsi(u[t], rec["psi_kind"])
         r = np.where(m_n != 0, g_u * np.sign(d[t]) / zeta_n, 0.0)
         lam = r + alpha * lam_next if stateful else r
-        gX[t] = lam
+        gX[t] = lam + dH[t][:, None] / B if rec["residual"] else lam   # B compartments: P = B
+        # H[t] = beta (1 - S[t-1]) H[t-1] + Z[t]: the PLIF soma's beta gradient
+        if t > 0:
+            t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]
         t_kappa[t] = np.where(m_n != 0, dH[t][:, None] * Y[t], 0.0)
         t_xi[t] = -r
         t_zeta[t] = np.where(m_n != 0, -g_u * u[t] / zeta_n, 0.0)
@@ -280,6 +292,8 @@ def backward(
         g_xi=_channel_sum(t_xi, batch, C, S),
         g_zeta=_channel_sum(t_zeta, batch, C, S),
         g_alpha=float(t_alpha.sum()),
+        g_beta=float(t_beta.sum()),
+        abs_beta=float(np.abs(t_beta).sum()),
         abs_kappa=_channel_sum(np.abs(t_kappa), batch, C, S),
         abs_xi=_channel_sum(np.abs(t_xi), batch, C, S),
         abs_zeta=_channel_sum(np.abs(t_zeta), batch, C, S),

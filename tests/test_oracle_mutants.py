@@ -28,6 +28,13 @@ MUTANTS = {
          'kstar_n = _per_neuron(rec["kappa"], batch, C, S)')],
     "g_zeta missing 1/zeta": ("-g_u * u[t] / zeta_n", "-g_u * u[t]"),
     "sigmoid surrogate scale dropped": ("return scale * s * (1.0 - s)", "return s * (1.0 - s)"),
+    "residual gradient dropped": ('gX[t] = lam + dH[t][:, None] / B if rec["residual"] else lam',
+                                  'gX[t] = lam'),
+    "residual uses the sum, not the mean": ("Z[t] = Z[t] + X[t].mean(axis=1)", "Z[t] = Z[t] + X[t].sum(axis=1)"),
+    "g_beta uses H[t] instead of H[t-1]": ("t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]",
+                                           "t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t]"),
+    "g_beta ignores the reset": ("t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]",
+                                 "t_beta[t] = dH[t] * H[t - 1]"),
     "stateless still leaks": ("Vd[t + 1] = alpha * Vd[t] + X[t] if stateful else X[t]",
                               "Vd[t + 1] = alpha * Vd[t] + X[t]"),
 }
@@ -41,9 +48,12 @@ PIN_CALLS = [
     lambda: pins.test_constant_drive_mexican_hat_zero_input(),
     lambda: pins.test_forward_matches_scalar_stepper("mexhat", True, True),
     lambda: pins.test_forward_matches_scalar_stepper("identity", False, False),
-    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True),
-    lambda: pins.test_backward_matches_autograd("identity", "atan", False, False, True),
+    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, False),
+    lambda: pins.test_backward_matches_autograd("identity", "atan", False, False, True, False),
     lambda: pins.test_mask_invariants(),
+    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, True),
+    lambda: pins.test_residual_with_zero_strengths_is_lif_of_the_mean_input(),
+    lambda: pins.test_plif_beta_gradient_of_a_free_leak(),
 ]
 
 

@@ -44,7 +44,7 @@ WORKED = dict(alpha=0.5, beta=0.5, v_th=1.0, kappa=np.array([[0.5, 0.25]]),
 
 
 def rand_case(rng, T=5, batch=2, C=3, S=2, B=3, psi_kind=PSI_MEXHAT, stateful=True,
-              mask=False, scale=1.0):
+              mask=False, scale=1.0, residual=False):
     N = batch * C * S
     X = rng.normal(0.0, scale, size=(T, N, B))
     kappa = rng.uniform(0.0, 1.0, size=(C, B)) + 0.3
@@ -54,14 +54,15 @@ def rand_case(rng, T=5, batch=2, C=3, S=2, B=3, psi_kind=PSI_MEXHAT, stateful=Tr
     gS = rng.normal(size=(T, N))
     gV = rng.normal(size=(T, N))
     return dict(X=X, kappa=kappa, xi=xi, zeta=zeta, mask=m, gS=gS, gV=gV, C=C, S=S,
-                psi_kind=psi_kind, stateful=stateful, alpha=0.6, beta=0.7, v_th=1.0)
+                psi_kind=psi_kind, stateful=stateful, alpha=0.6, beta=0.7, v_th=1.0, residual=residual)
 
 
 def run_oracle(case, force=None):
     return oracle.forward(case["X"], alpha=case["alpha"], beta=case["beta"], v_th=case["v_th"],
                           kappa=case["kappa"], xi=case["xi"], zeta=case["zeta"],
                           mask=case["mask"], C=case["C"], S=case["S"],
-                          psi_kind=case["psi_kind"], stateful=case["stateful"], force=force)
+                          psi_kind=case["psi_kind"], stateful=case["stateful"],
+                          residual=case.get("residual", False), force=force)
 
 
 # ---------------------------------------------------------------------------
@@ -102,6 +103,8 @@ def test_worked_example_backward_by_hand():
     # g_kappa = sum_t dH[t] Y[t]
     gk = dH1 * np.array([1, 2]) + dH2 * np.array([1, 0]) + dH3 * np.array([2.5, 0])
     assert np.allclose(g["g_kappa"][0], gk, rtol=1e-14)
+    # g_beta = sum_t dH[t] (1 - S[t-1]) H[t-1]: only t = 3 counts (S[1] = 1 resets step 2)
+    assert math.isclose(g["g_beta"], dH3 * 0.5, rel_tol=1e-14)
 
 
 # ---------------------------------------------------------------------------
@@ -355,6 +358,7 @@ def autograd_grads(case, sg_kind, sg_scale, detach_reset):
     zeta = torch.tensor(case["zeta"] if case["zeta"] is not None else np.ones((C, B)),
                         dtype=torch_dtype, requires_grad=True)
     alpha = torch.tensor(case["alpha"], dtype=torch_dtype, requires_grad=True)
+    beta = torch.tensor(case["beta"], dtype=torch_dtype, requires_grad=True)
     m = torch.tensor(np.ones((C, B)) if case["mask"] is None else (case["mask"] != 0) * 1.0,
                      dtype=torch_dtype)
 
@@ -386,14 +390,17 @@ def autograd_grads(case, sg_kind, sg_scale, detach_reset):
         uu = torch.abs(vd - per_neuron(xi)) / per_neuron(zeta)
         y = (1 - uu ** 2) * torch.exp(-uu ** 2 / 2) if case["psi_kind"] == PSI_MEXHAT else uu
         z = (per_neuron(kappa * m) * y).sum(dim=1)
+        if case.get("residual", False):
+            z = z + X[t].mean(dim=1)
         reset = s.detach() if detach_reset else s
-        h = case["beta"] * (1 - reset) * h + z
+        h = beta * (1 - reset) * h + z
         s = Spike.apply(h - case["v_th"])
         loss = loss + (gS[t] * s).sum() + (gV[t] * h).sum()
     loss.backward()
     ga = 0.0 if alpha.grad is None else float(alpha.grad)
+    gb = 0.0 if beta.grad is None else float(beta.grad)
     return dict(gX=X.grad.numpy(), g_kappa=kappa.grad.numpy(), g_xi=xi.grad.numpy(),
-                g_zeta=zeta.grad.numpy(), g_alpha=ga)
+                g_zeta=zeta.grad.numpy(), g_alpha=ga, g_beta=gb)
 
 
 @pytest.mark.parametrize("sg_kind", [SG_ATAN, SG_SIGMOID])
@@ -412,11 +419,13 @@ def test_worked_example_backward_vs_autograd(sg_kind, detach_reset):
 @pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
 @pytest.mark.parametrize("sg_kind", [SG_ATAN, SG_SIGMOID])
 @pytest.mark.parametrize("detach_reset", [False, True])
-@pytest.mark.parametrize("stateful,mask", [(True, False), (True, True), (False, True)])
-def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, mask):
+@pytest.mark.parametrize("stateful,mask,residual", [(True, False, False), (True, True, False),
+                                                   (False, True, False), (True, True, True),
+                                                   (False, False, True)])
+def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, mask, residual):
     rng = np.random.default_rng(8)
     case = rand_case(rng, T=6, batch=2, C=3, S=2, B=3, psi_kind=psi_kind, stateful=stateful,
-                     mask=mask, scale=1.2)
+                     mask=mask, scale=1.2, residual=residual)
     rec = run_oracle(case)
     g = oracle.backward(rec, case["gS"], case["gV"], sg_kind=sg_kind, sg_scale=3.0,
                         detach_reset=detach_reset)
@@ -424,6 +433,7 @@ def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, ma
     for k in ("gX", "g_kappa", "g_xi", "g_zeta"):
         assert np.allclose(g[k], a[k], rtol=1e-11, atol=1e-13), k
     assert math.isclose(g["g_alpha"], a["g_alpha"], rel_tol=1e-11, abs_tol=1e-13)
+    assert math.isclose(g["g_beta"], a["g_beta"], rel_tol=1e-11, abs_tol=1e-13)
     if mask:
         off = case["mask"] == 0
         for k in ("g_kappa", "g_xi", "g_zeta"):
@@ -434,7 +444,7 @@ def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, ma
 # Backward against central finite differences of a smooth forward
 # ---------------------------------------------------------------------------
 def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None, xi=None,
-                zeta=None, alpha=None):
+                zeta=None, alpha=None, beta=None):
     """Loss sum(gS S~) + sum(gV H) of a forward whose spike is
     S~[t] = S_base[t] + F(H[t] - v_th) - F(H_base[t] - v_th), F the surrogate's
     primitive.  At the base point S~ equals the recorded spikes, so the
@@ -447,6 +457,7 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
     xi = case["xi"] if xi is None else xi
     zeta = case["zeta"] if zeta is None else zeta
     alpha = case["alpha"] if alpha is None else alpha
+    beta = case["beta"] if beta is None else beta
     T, N, B = X.shape
     C, S = case["C"], case["S"]
     m = np.ones((C, B)) if case["mask"] is None else (case["mask"] != 0) * 1.0
@@ -465,7 +476,9 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
         uu = np.abs(vd - xi[cidx]) / zeta[cidx]
         y = (1 - uu * uu) * np.exp(-0.5 * uu * uu) if case["psi_kind"] == PSI_MEXHAT else uu
         z = ((kappa * m)[cidx] * y).sum(axis=1)
-        h = case["beta"] * (1 - (s_b if detach_reset else s_t)) * h + z
+        if case.get("residual", False):
+            z = z + X[t].sum(axis=1) / B
+        h = beta * (1 - (s_b if detach_reset else s_t)) * h + z
         s_t = base["S"][t] + F(h - case["v_th"]) - F(base["H"][t] - case["v_th"])
         s_b = base["S"][t]
         loss += np.sum(case["gS"][t] * s_t) + np.sum(case["gV"][t] * h)
@@ -475,9 +488,11 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
 @pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
 @pytest.mark.parametrize("sg_kind", [SG_ATAN, SG_SIGMOID])
 @pytest.mark.parametrize("detach_reset", [False, True])
-def test_backward_matches_finite_differences(psi_kind, sg_kind, detach_reset):
+@pytest.mark.parametrize("residual", [False, True])
+def test_backward_matches_finite_differences(psi_kind, sg_kind, detach_reset, residual):
     rng = np.random.default_rng(9)
-    case = rand_case(rng, T=4, batch=1, C=2, S=2, B=3, psi_kind=psi_kind, mask=True, scale=1.2)
+    case = rand_case(rng, T=4, batch=1, C=2, S=2, B=3, psi_kind=psi_kind, mask=True, scale=1.2,
+                     residual=residual)
     rec = run_oracle(case)
     g = oracle.backward(rec, case["gS"], case["gV"], sg_kind=sg_kind, sg_scale=4.0,
                         detach_reset=detach_reset)
@@ -502,6 +517,8 @@ def test_backward_matches_finite_differences(psi_kind, sg_kind, detach_reset):
         assert np.allclose(g[key], num, rtol=1e-6, atol=1e-7 * scale), name
     num_a = (L(alpha=case["alpha"] + eps) - L(alpha=case["alpha"] - eps)) / (2 * eps)
     assert math.isclose(g["g_alpha"], num_a, rel_tol=1e-6, abs_tol=1e-8)
+    num_b = (L(beta=case["beta"] + eps) - L(beta=case["beta"] - eps)) / (2 * eps)
+    assert math.isclose(g["g_beta"], num_b, rel_tol=1e-6, abs_tol=1e-8)
 
 
 # ---------------------------------------------------------------------------
@@ -609,3 +626,56 @@ def test_forced_spikes_override_decision():
     others = np.ones(rec["S"].shape[1], dtype=bool)
     others[0] = False
     assert np.array_equal(r2["S"][:, others], rec["S"][:, others])
+
+
+# ---------------------------------------------------------------------------
+# Residual dendrite (Eq. methods-residual)
+# ---------------------------------------------------------------------------
+def test_residual_with_zero_strengths_is_lif_of_the_mean_input():
+    """kappa = 0: the soma sees only (1/P) sum_i X_i, so the layer is a LIF neuron
+    driven by the mean input (bit for bit against the textbook LIF on that mean)."""
+    rng = np.random.default_rng(20)
+    T, N, B = 12, 5, 4
+    X = rng.normal(0.4, 1.0, size=(T, N, B))
+    rec = oracle.forward(X, alpha=0.6, beta=0.8, v_th=1.0, kappa=np.zeros((N, B)), C=N,
+                         psi_kind=PSI_MEXHAT, residual=True)
+    for n in range(N):
+        v, s = textbook_lif(X[:, n, :].mean(axis=1), 0.8, 1.0)
+        assert np.array_equal(rec["H"][:, n], v)
+        assert np.array_equal(rec["S"][:, n], s)
+
+
+@pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
+def test_residual_single_step_closed_form(psi_kind):
+    rng = np.random.default_rng(21)
+    case = rand_case(rng, T=1, psi_kind=psi_kind, mask=True, residual=True)
+    case["gV"] = np.zeros_like(case["gV"])
+    rec = run_oracle(case)
+    base = dict(case, residual=False)
+    rec0 = run_oracle(base)
+    B = case["X"].shape[2]
+    assert np.allclose(rec["H"][0], rec0["H"][0] + case["X"][0].mean(axis=1), rtol=1e-14, atol=1e-15)
+    g = oracle.backward(rec, case["gS"], sg_kind=SG_ATAN)
+    g0 = oracle.backward(rec0, case["gS"], sg_kind=SG_ATAN)
+    sg = 1.0 / (1.0 + (math.pi * (rec["H"][0] - 1.0)) ** 2)
+    sg0 = 1.0 / (1.0 + (math.pi * (rec0["H"][0] - 1.0)) ** 2)
+    dH = sg * case["gS"][0]
+    # the dendritic part scales with dH; the residual part adds dH / P to every compartment
+    expect = g0["gX"][0] * (dH / np.where(sg0 * case["gS"][0] == 0, 1, sg0 * case["gS"][0]))[:, None] + dH[:, None] / B
+    assert np.allclose(g["gX"][0], expect, rtol=1e-11, atol=1e-13)
+
+
+def test_plif_beta_gradient_of_a_free_leak():
+    """No input after the first step, no spikes: H[t] = beta^(t-1) z for t >= 1, so with
+    gV = 1 at the last step only and the reset path detached (no surrogate term),
+    dL/dbeta = (T-1) beta^(T-2) z (textbook derivative)."""
+    T, beta, z = 6, 0.7, 0.6
+    X = np.zeros((T, 1, 1))
+    X[0, 0, 0] = z
+    rec = oracle.forward(X, alpha=0.0, beta=beta, v_th=10.0, kappa=np.ones((1, 1)), C=1,
+                         psi_kind=PSI_IDENTITY, stateful=False)
+    gV = np.zeros((T, 1))
+    gV[-1, 0] = 1.0
+    g = oracle.backward(rec, np.zeros((T, 1)), gV, sg_kind=SG_ATAN, detach_reset=True)
+    assert math.isclose(rec["H"][-1, 0], beta ** (T - 1) * z, rel_tol=1e-14)
+    assert math.isclose(g["g_beta"], (T - 1) * beta ** (T - 2) * z, rel_tol=1e-13)
