@@ -167,6 +167,7 @@ def main():
     ckpt = torch.empty((max(1, nck_bytes // 4),), dtype=torch.float32, device=dev) if nck_bytes else None
     gX = torch.empty_like(X)
     g_alpha = torch.empty((1,), dtype=torch.float32, device=dev)
+    g_beta = torch.empty((1,), dtype=torch.float32, device=dev)
     g_kappa = torch.empty_like(kappa)
     g_xi = torch.empty_like(kappa)
     g_zeta = torch.empty_like(kappa)
@@ -177,9 +178,9 @@ def main():
     def step():
         # one step: forward + backward of the layer (every task's mask for the gated layer)
         for m in tasks:
-            dendsn.dendsn_forward(cfg, X, alpha, kappa, None, None, m, spikes, None, ckpt)
-            dendsn.dendsn_backward(cfg, X, alpha, kappa, None, None, m, ckpt, gS, None, gX, g_alpha, g_kappa,
-                                   g_xi, g_zeta, ws)
+            dendsn.dendsn_forward(cfg, X, alpha, None, kappa, None, None, m, spikes, None, ckpt)
+            dendsn.dendsn_backward(cfg, X, alpha, None, kappa, None, None, m, ckpt, gS, None, gX, g_alpha,
+                                   g_beta, g_kappa, g_xi, g_zeta, ws)
 
     for _ in range(args.warmup):
         step()
@@ -204,10 +205,10 @@ def main():
         for m in tasks:
             e = next(it)
             e[0].record(stream)
-            dendsn.dendsn_forward(cfg, X, alpha, kappa, None, None, m, spikes, None, ckpt)
+            dendsn.dendsn_forward(cfg, X, alpha, None, kappa, None, None, m, spikes, None, ckpt)
             e[1].record(stream)
-            dendsn.dendsn_backward(cfg, X, alpha, kappa, None, None, m, ckpt, gS, None, gX, g_alpha, g_kappa,
-                                   g_xi, g_zeta, ws)
+            dendsn.dendsn_backward(cfg, X, alpha, None, kappa, None, None, m, ckpt, gS, None, gX, g_alpha,
+                                   g_beta, g_kappa, g_xi, g_zeta, ws)
             e[2].record(stream)
     torch.cuda.synchronize(dev)
     fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / len(evs)

@@ -13,7 +13,11 @@
  *     Eq. (methods-soma-input)         Z[t]    = sum_b kappa_b Y_b[t]
  *     Eq. (methods-lif-reset-charge)   H[t]    = beta (1 - S[t-1]) H[t-1] + Z[t],  H[0] = S[0] = 0
  *     Eq. (methods-lif-fire)           S[t]    = 1 if H[t] - v_th >= 0 else 0
- *   Methods, "DendSN variants": Stateless Dendrite (Vd_b[t] = X_b[t]).
+ *   Methods, "DendSN variants": Stateless Dendrite (Vd_b[t] = X_b[t]) and the
+ *     residual dendrite, Eq. (methods-residual): Z[t] += (1/P) sum_i X_i[t]
+ *     (ResStateful / ResStateless).
+ *   Methods, "Dendritic spiking neuron", soma: a LIF soma with a fixed decay, or
+ *     the parametric LIF (PLIF) soma, whose decay beta is learnable.
  *   Methods, "Dendritic branch gating": kappa* = kappa (.) m with a fixed binary
  *     mask m per task, Eq. (methods-dbg-mask) and Eq. (methods-dbg-sampling).
  *   Methods, "Dendritic spiking neural networks": layer form — neurons of one
@@ -27,6 +31,8 @@
  *   kappa, xi, zeta    [C, B]     fp32 per-channel parameters
  *   mask               [C, B]     uint8, nonzero = branch kept
  *   alpha              [1]        fp32 on the device (a learnable layer scalar)
+ *   beta               [1]        fp32 on the device, optional: a learnable somatic decay
+ *                                 (PLIF); NULL uses cfg->beta
  *   Neuron n = (b_idx * C + c) * S + s for batch item b_idx, channel c, spatial
  *   position s; a fully connected layer has S = 1.
  *
@@ -87,6 +93,7 @@ typedef struct dendsn_cfg {
     float beta;                /* somatic decay, 0 <= beta < 1                              */
     float v_th;                /* firing threshold (the paper uses 1)                       */
     int32_t batch_groups;      /* tuning: batch groups per launch, 0 = automatic           */
+    int32_t residual;          /* 1: residual dendrite, Z += mean of the neuron's inputs   */
 } dendsn_cfg;
 
 /*
@@ -108,7 +115,9 @@ dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes);
  * Forward scan over t = 1..T (equations above).
  *   x       [T,N,B] io    required
  *   alpha   [1] fp32      required when cfg->stateful, ignored otherwise
- *   kappa   [C,B] fp32    required
+ *   beta    [1] fp32      optional learnable somatic decay (NULL: cfg->beta)
+ *   kappa   [C,B] fp32    required (for dendritic branch gating with per-task dense
+ *                         strengths, DBG_e, pass the task's own [C,B] table)
  *   xi      [C,B] fp32    NULL means 0
  *   zeta    [C,B] fp32    NULL means 1
  *   mask    [C,B] uint8   NULL means every branch kept
@@ -118,21 +127,24 @@ dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes);
  *           inference (no backward will follow), or when K >= T.
  */
 dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* alpha,
-                             const float* kappa, const float* xi, const float* zeta,
-                             const uint8_t* mask, void* spikes, float* v_soma, float* ckpt,
-                             hipStream_t stream);
+                             const float* beta, const float* kappa, const float* xi,
+                             const float* zeta, const uint8_t* mask, void* spikes, float* v_soma,
+                             float* ckpt, hipStream_t stream);
 
 /*
  * Backward scan: gradients of  sum(grad_spikes * S) + sum(grad_v_soma * H)  with
  * Theta'(H - v_th) replaced by the surrogate cfg->sg, through time (BPTT).
  * The dendrite is recomputed from x and the checkpoints (gradient
  * checkpointing); nothing else of the forward is stored.  The call must use the
- * same cfg, x, alpha, kappa, xi, zeta and mask as the forward that wrote ckpt.
+ * same cfg, x, alpha, beta, kappa, xi, zeta and mask as the forward that wrote ckpt.
  *   ckpt         required when nck > 0 (see dendsn_ckpt_bytes)
  *   grad_spikes  [T,N] io     required
  *   grad_v_soma  [T,N] fp32   NULL means 0
- *   grad_x       [T,N,B] io   required output
+ *   grad_x       [T,N,B] io   required output (with the residual dendrite it includes the
+ *                dH/P of the residual path, also on gated-off branches)
  *   grad_alpha   [1] fp32     optional output (0 for the Stateless Dendrite)
+ *   grad_beta    [1] fp32     optional output: d/d beta of the loss (PLIF soma), summed
+ *                over time and neurons; meaningful whether beta came from cfg or the device
  *   grad_kappa, grad_xi, grad_zeta  [C,B] fp32 optional outputs, summed over
  *                time, batch and spatial positions; exactly 0 where the mask is 0.
  *   workspace    device scratch of at least dendsn_bwd_workspace_bytes bytes,
@@ -140,11 +152,12 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
  * Results are deterministic: the same inputs give bit-identical outputs.
  */
 dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha,
-                              const float* kappa, const float* xi, const float* zeta,
-                              const uint8_t* mask, const float* ckpt, const void* grad_spikes,
-                              const float* grad_v_soma, void* grad_x, float* grad_alpha,
-                              float* grad_kappa, float* grad_xi, float* grad_zeta,
-                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+                              const float* beta, const float* kappa, const float* xi,
+                              const float* zeta, const uint8_t* mask, const float* ckpt,
+                              const void* grad_spikes, const float* grad_v_soma, void* grad_x,
+                              float* grad_alpha, float* grad_beta, float* grad_kappa,
+                              float* grad_xi, float* grad_zeta, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
 
 /* Static name of a status code. */
 const char* dendsn_status_str(dendsn_status status);

@@ -49,6 +49,7 @@ class dendsn_cfg(ctypes.Structure):
         ("beta", ctypes.c_float),
         ("v_th", ctypes.c_float),
         ("batch_groups", ctypes.c_int32),
+        ("residual", ctypes.c_int32),
     ]
 
 
@@ -72,6 +73,7 @@ class DendSNConfig:
     v_th: float = 1.0
     batch_groups: int = 0
     comps_per_branch: int = 1
+    residual: bool = False
 
     @property
     def N(self) -> int:
@@ -87,7 +89,7 @@ class DendSNConfig:
             detach_reset=int(self.detach_reset),
             ckpt_every=self.ckpt_every if self.ckpt_every > 0 else max(1, min(self.T, 2**31 - 1)),
             io=IO[self.io], psi=PSI[self.psi], sg=SG[self.sg], sg_scale=self.sg_scale,
-            beta=self.beta, v_th=self.v_th, batch_groups=self.batch_groups,
+            beta=self.beta, v_th=self.v_th, batch_groups=self.batch_groups, residual=int(self.residual),
         )
 
 
@@ -96,8 +98,8 @@ _lib = None
 _SIGS = {
     "dendsn_ckpt_bytes": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg), ctypes.POINTER(ctypes.c_size_t)]),
     "dendsn_bwd_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg), ctypes.POINTER(ctypes.c_size_t)]),
-    "dendsn_forward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 10),
-    "dendsn_backward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 15
+    "dendsn_forward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 11),
+    "dendsn_backward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 17
                         + [ctypes.c_size_t, ctypes.c_void_p]),
     "dendsn_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "dendsn_last_error": (ctypes.c_char_p, []),
@@ -161,22 +163,24 @@ def dendsn_bwd_workspace_bytes(cfg: DendSNConfig) -> int:
     return out.value
 
 
-def dendsn_forward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, spikes, v_soma, ckpt, stream=None):
+def dendsn_forward(cfg: DendSNConfig, x, alpha, beta, kappa, xi, zeta, mask, spikes, v_soma, ckpt,
+                   stream=None):
     c = cfg.to_c()
     st = stream if stream is not None else _stream(x.device)
-    _check(lib().dendsn_forward(ctypes.byref(c), _ptr(x), _ptr(alpha), _ptr(kappa), _ptr(xi), _ptr(zeta),
-                                _ptr(mask), _ptr(spikes), _ptr(v_soma), _ptr(ckpt), st))
+    _check(lib().dendsn_forward(ctypes.byref(c), _ptr(x), _ptr(alpha), _ptr(beta), _ptr(kappa), _ptr(xi),
+                                _ptr(zeta), _ptr(mask), _ptr(spikes), _ptr(v_soma), _ptr(ckpt), st))
 
 
-def dendsn_backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma,
-                    grad_x, grad_alpha, grad_kappa, grad_xi, grad_zeta, workspace, stream=None):
+def dendsn_backward(cfg: DendSNConfig, x, alpha, beta, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma,
+                    grad_x, grad_alpha, grad_beta, grad_kappa, grad_xi, grad_zeta, workspace, stream=None):
     c = cfg.to_c()
     st = stream if stream is not None else _stream(x.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().dendsn_backward(ctypes.byref(c), _ptr(x), _ptr(alpha), _ptr(kappa), _ptr(xi), _ptr(zeta),
-                                 _ptr(mask), _ptr(ckpt), _ptr(grad_spikes), _ptr(grad_v_soma), _ptr(grad_x),
-                                 _ptr(grad_alpha), _ptr(grad_kappa), _ptr(grad_xi), _ptr(grad_zeta),
-                                 _ptr(workspace), ctypes.c_size_t(ws_bytes), st))
+    _check(lib().dendsn_backward(ctypes.byref(c), _ptr(x), _ptr(alpha), _ptr(beta), _ptr(kappa), _ptr(xi),
+                                 _ptr(zeta), _ptr(mask), _ptr(ckpt), _ptr(grad_spikes), _ptr(grad_v_soma),
+                                 _ptr(grad_x), _ptr(grad_alpha), _ptr(grad_beta), _ptr(grad_kappa),
+                                 _ptr(grad_xi), _ptr(grad_zeta), _ptr(workspace), ctypes.c_size_t(ws_bytes),
+                                 st))
 
 
 # ---------------------------------------------------------------------------
@@ -203,46 +207,49 @@ def _expect(t, name, shape, dtype, device, optional=False):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _check_params(cfg, x, alpha, kappa, xi, zeta, mask):
+def _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta=None):
     import torch
 
     dev = x.device
     _expect(x, "x", (cfg.T, cfg.N, cfg.B), _io_dtype(cfg), dev)
     _expect(alpha, "alpha", (1,), torch.float32, dev, optional=not cfg.stateful)
+    _expect(beta, "beta", (1,), torch.float32, dev, optional=True)
     _expect(kappa, "kappa", (cfg.C, cfg.B), torch.float32, dev)
     _expect(xi, "xi", (cfg.C, cfg.B), torch.float32, dev, optional=True)
     _expect(zeta, "zeta", (cfg.C, cfg.B), torch.float32, dev, optional=True)
     _expect(mask, "mask", (cfg.C, cfg.B), torch.uint8, dev, optional=True)
 
 
-def forward(cfg: DendSNConfig, x, alpha, kappa, xi=None, zeta=None, mask=None, *,
+def forward(cfg: DendSNConfig, x, alpha, kappa, xi=None, zeta=None, mask=None, *, beta=None,
             want_v_soma: bool = False, save_ckpt: bool = True):
-    """Returns (spikes [T,N] io, v_soma [T,N] fp32 or None, ckpt buffer or None)."""
+    """Returns (spikes [T,N] io, v_soma [T,N] fp32 or None, ckpt buffer or None).
+    ``beta``: optional learnable somatic decay [1] on the device (else cfg.beta)."""
     import torch
 
-    _check_params(cfg, x, alpha, kappa, xi, zeta, mask)
+    _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta)
     dev = x.device
     spikes = torch.empty((cfg.T, cfg.N), dtype=_io_dtype(cfg), device=dev)
     v_soma = torch.empty((cfg.T, cfg.N), dtype=torch.float32, device=dev) if want_v_soma else None
     nb = dendsn_ckpt_bytes(cfg)
     ckpt = torch.empty((nb // 4,), dtype=torch.float32, device=dev) if (save_ckpt and nb) else None
-    dendsn_forward(cfg, x, alpha, kappa, xi, zeta, mask, spikes, v_soma, ckpt)
+    dendsn_forward(cfg, x, alpha, beta, kappa, xi, zeta, mask, spikes, v_soma, ckpt)
     return spikes, v_soma, ckpt
 
 
 def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma=None,
-             workspace=None):
-    """Returns a dict with grad_x [T,N,B] io and grad_alpha [1], grad_kappa,
-    grad_xi, grad_zeta [C,B] (fp32)."""
+             workspace=None, *, beta=None):
+    """Returns a dict with grad_x [T,N,B] io and grad_alpha [1], grad_beta [1],
+    grad_kappa, grad_xi, grad_zeta [C,B] (fp32)."""
     import torch
 
-    _check_params(cfg, x, alpha, kappa, xi, zeta, mask)
+    _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta)
     dev = x.device
     _expect(grad_spikes, "grad_spikes", (cfg.T, cfg.N), _io_dtype(cfg), dev)
     _expect(grad_v_soma, "grad_v_soma", (cfg.T, cfg.N), torch.float32, dev, optional=True)
     out = dict(
         grad_x=torch.empty((cfg.T, cfg.N, cfg.B), dtype=_io_dtype(cfg), device=dev),
         grad_alpha=torch.empty((1,), dtype=torch.float32, device=dev),
+        grad_beta=torch.empty((1,), dtype=torch.float32, device=dev),
         grad_kappa=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
         grad_xi=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
         grad_zeta=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
@@ -250,7 +257,7 @@ def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spik
     if workspace is None:
         nb = dendsn_bwd_workspace_bytes(cfg)
         workspace = torch.empty(((nb + 3) // 4,), dtype=torch.float32, device=dev)
-    dendsn_backward(cfg, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma,
-                    out["grad_x"], out["grad_alpha"], out["grad_kappa"], out["grad_xi"],
+    dendsn_backward(cfg, x, alpha, beta, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma,
+                    out["grad_x"], out["grad_alpha"], out["grad_beta"], out["grad_kappa"], out["grad_xi"],
                     out["grad_zeta"], workspace)
     return out

@@ -21,17 +21,22 @@ hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int psi, hipStream
 __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   const int tid = threadIdx.x;
   const int64_t nout = f.C * 3 * f.B;
-  if (blockIdx.x == gridDim.x - 1) {
+  if (blockIdx.x >= gridDim.x - 2) {  // last block: g_alpha; the one before: g_beta
+    const bool is_alpha = blockIdx.x == gridDim.x - 1;
+    const float* src = is_alpha ? f.wsA : f.wsB;
     __shared__ double sh[kThreads];
     double s = 0.0;
-    for (int64_t i = tid; i < f.nA; i += kThreads) s += double(f.wsA[i]);
+    for (int64_t i = tid; i < f.nA; i += kThreads) s += double(src[i]);
     sh[tid] = s;
     __syncthreads();
     for (int w = kThreads / 2; w >= 1; w >>= 1) {
       if (tid < w) sh[tid] += sh[tid + w];
       __syncthreads();
     }
-    if (tid == 0 && f.ga) f.ga[0] = f.stateful ? float(sh[0]) : 0.0f;
+    if (tid == 0) {
+      if (is_alpha && f.ga) f.ga[0] = f.stateful ? float(sh[0]) : 0.0f;
+      if (!is_alpha && f.gb) f.gb[0] = float(sh[0]);
+    }
     return;
   }
   int64_t o;
@@ -93,17 +98,6 @@ bool choose_mapping(int B, int io, int* BL, int* L, int* fast) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// The backward's lane split.  Any power-of-two split of a power-of-two
-// per-lane count adds the branch terms in the same pairwise tree (in-lane pairs,
-// then DPP pairs), so the backward may hold fewer branches per lane than the
-// forward (fewer stash registers, more waves) and still recompute the forward's
-// exact bits.  Generic splits (sequential in-lane sums) must match the forward.
-void bwd_mapping(int B, int io, int* BL, int* L, int* fast) {
-  choose_mapping(B, io, BL, L, fast);
-  (void)B;
-  (void)io;
-}
-
 dendsn_status check_cfg(const dendsn_cfg* c) {
   if (!c) return fail(DENDSN_E_INVALID, "cfg is NULL");
   if (c->T < 1 || c->T > INT32_MAX) return fail(DENDSN_E_INVALID, "T must be in [1, 2^31)");
@@ -126,6 +120,7 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   if (!isfinite(c->beta)) return fail(DENDSN_E_INVALID, "beta must be finite");
   if (!isfinite(c->v_th)) return fail(DENDSN_E_INVALID, "v_th must be finite");
   if (c->batch_groups < 0) return fail(DENDSN_E_INVALID, "batch_groups must be >= 0");
+  if (c->residual != 0 && c->residual != 1) return fail(DENDSN_E_INVALID, "residual must be 0 or 1");
   // N and T * N * B must fit comfortably in int64 element counts.
   const int64_t lim = int64_t(1) << 46;
   if (c->batch > lim / c->C || c->batch * c->C > lim / c->S) return fail(DENDSN_E_INVALID, "N too large");
@@ -142,10 +137,7 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
 Plan make_plan(const dendsn_cfg* c, bool bwd) {
   Plan p;
   memset(&p, 0, sizeof(p));
-  if (bwd)
-    bwd_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
-  else
-    choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
+  choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
   const int L = p.L;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
@@ -188,7 +180,7 @@ void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) 
   const size_t nP = size_t(p.G) * size_t(p.tpc) * size_t(c->C) * 3 * size_t(c->B);
   const size_t nA = size_t(p.G) * size_t(p.ntiles);
   *offA = ((nP * sizeof(float) + 255) / 256) * 256;
-  *total = *offA + nA * sizeof(float);
+  *total = *offA + 2 * nA * sizeof(float);  // g_alpha partials, then g_beta partials
 }
 
 dendsn_status check_grid(const dendsn_cfg* c, const Plan& p) {
@@ -200,10 +192,12 @@ dendsn_status check_grid(const dendsn_cfg* c, const Plan& p) {
   return DENDSN_OK;
 }
 
-void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* alpha, const float* kappa,
-               const float* xi, const float* zeta, const uint8_t* mask, ScanArgs* s) {
+void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* alpha, const float* beta,
+               const float* kappa, const float* xi, const float* zeta, const uint8_t* mask, ScanArgs* s) {
   s->x = x;
   s->alpha = c->stateful ? alpha : nullptr;
+  s->beta_p = beta;
+  s->rP = 1.0f / float(c->B * c->comps_per_branch);
   s->kappa = kappa; s->xi = xi; s->zeta = zeta; s->mask = mask;
   s->T = c->T; s->C = c->C; s->S = c->S; s->batch = c->batch;
   s->M = c->C * c->S; s->N = c->batch * s->M;
@@ -252,9 +246,9 @@ dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes) {
   return DENDSN_OK;
 }
 
-dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* kappa,
-                             const float* xi, const float* zeta, const uint8_t* mask, void* spikes,
-                             float* v_soma, float* ckpt, hipStream_t stream) {
+dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* beta,
+                             const float* kappa, const float* xi, const float* zeta, const uint8_t* mask,
+                             void* spikes, float* v_soma, float* ckpt, hipStream_t stream) {
   g_last_error.clear();
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
@@ -266,28 +260,30 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   if (!aligned(x, 16)) return fail(DENDSN_E_INVALID, "x must be 16-byte aligned");
   if (!aligned(spikes, esz)) return fail(DENDSN_E_INVALID, "spikes misaligned");
   if (ckpt && !aligned(ckpt, 16)) return fail(DENDSN_E_INVALID, "ckpt must be 16-byte aligned");
-  if ((alpha && !aligned(alpha, 4)) || !aligned(kappa, 4) || (xi && !aligned(xi, 4)) ||
-      (zeta && !aligned(zeta, 4)) || (v_soma && !aligned(v_soma, 4)))
+  if ((alpha && !aligned(alpha, 4)) || (beta && !aligned(beta, 4)) || !aligned(kappa, 4) ||
+      (xi && !aligned(xi, 4)) || (zeta && !aligned(zeta, 4)) || (v_soma && !aligned(v_soma, 4)))
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
   const Plan p = make_plan(cfg, false);
   if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
   FwdArgs fa;
   memset(&fa, 0, sizeof(fa));
-  fill_scan(cfg, p, x, alpha, kappa, xi, zeta, mask, &fa.s);
+  fill_scan(cfg, p, x, alpha, beta, kappa, xi, zeta, mask, &fa.s);
   fa.spikes = spikes;
   fa.vsoma = v_soma;
   fa.ckpt = p.nck > 0 ? ckpt : nullptr;
-  const hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_fwd_bf16(p, fa, cfg->psi, stream)
-                                                 : launch_fwd_f32(p, fa, cfg->psi, stream);
+  const int v = cfg->psi | (cfg->residual << 1);
+  const hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_fwd_bf16(p, fa, v, stream)
+                                                 : launch_fwd_f32(p, fa, v, stream);
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("forward launch: ") + hipGetErrorString(e));
   return DENDSN_OK;
 }
 
-dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* kappa,
-                              const float* xi, const float* zeta, const uint8_t* mask, const float* ckpt,
-                              const void* grad_spikes, const float* grad_v_soma, void* grad_x,
-                              float* grad_alpha, float* grad_kappa, float* grad_xi, float* grad_zeta,
-                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* beta,
+                              const float* kappa, const float* xi, const float* zeta, const uint8_t* mask,
+                              const float* ckpt, const void* grad_spikes, const float* grad_v_soma,
+                              void* grad_x, float* grad_alpha, float* grad_beta, float* grad_kappa,
+                              float* grad_xi, float* grad_zeta, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
   g_last_error.clear();
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
@@ -302,9 +298,10 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   if (!aligned(x, 16) || !aligned(grad_x, 16)) return fail(DENDSN_E_INVALID, "x / grad_x must be 16-byte aligned");
   if (ckpt && !aligned(ckpt, 16)) return fail(DENDSN_E_INVALID, "ckpt must be 16-byte aligned");
   if (!aligned(grad_spikes, esz)) return fail(DENDSN_E_INVALID, "grad_spikes misaligned");
-  if ((alpha && !aligned(alpha, 4)) || !aligned(kappa, 4) || (xi && !aligned(xi, 4)) ||
-      (zeta && !aligned(zeta, 4)) || (grad_v_soma && !aligned(grad_v_soma, 4)) ||
-      (grad_alpha && !aligned(grad_alpha, 4)) || (grad_kappa && !aligned(grad_kappa, 4)) ||
+  if ((alpha && !aligned(alpha, 4)) || (beta && !aligned(beta, 4)) || !aligned(kappa, 4) ||
+      (xi && !aligned(xi, 4)) || (zeta && !aligned(zeta, 4)) || (grad_v_soma && !aligned(grad_v_soma, 4)) ||
+      (grad_alpha && !aligned(grad_alpha, 4)) || (grad_beta && !aligned(grad_beta, 4)) ||
+      (grad_kappa && !aligned(grad_kappa, 4)) ||
       (grad_xi && !aligned(grad_xi, 4)) || (grad_zeta && !aligned(grad_zeta, 4)))
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
   size_t offA, total;
@@ -317,30 +314,32 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
 
   BwdArgs ba;
   memset(&ba, 0, sizeof(ba));
-  fill_scan(cfg, p, x, alpha, kappa, xi, zeta, mask, &ba.s);
+  fill_scan(cfg, p, x, alpha, beta, kappa, xi, zeta, mask, &ba.s);
   ba.ckpt = ckpt;
   ba.gspk = grad_spikes;
   ba.gv = grad_v_soma;
   ba.gx = grad_x;
   ba.wsP = static_cast<float*>(workspace);
   ba.wsA = reinterpret_cast<float*>(static_cast<char*>(workspace) + offA);
+  ba.wsB = ba.wsA + int64_t(p.G) * p.ntiles;
   ba.P = int64_t(p.G) * p.tpc;
   ba.wide = ba.P > kNarrowSlots;
   ba.detach = cfg->detach_reset;
   ba.sg = cfg->sg;
   ba.sg_scale = cfg->sg_scale;
-  hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_bwd_bf16(p, ba, cfg->psi, stream)
-                                           : launch_bwd_f32(p, ba, cfg->psi, stream);
+  const int v = cfg->psi | (cfg->residual << 1);
+  hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_bwd_bf16(p, ba, v, stream)
+                                           : launch_bwd_f32(p, ba, v, stream);
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("backward launch: ") + hipGetErrorString(e));
 
   FinArgs f;
   memset(&f, 0, sizeof(f));
-  f.wsP = ba.wsP; f.wsA = ba.wsA; f.mask = mask;
-  f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha;
+  f.wsP = ba.wsP; f.wsA = ba.wsA; f.wsB = ba.wsB; f.mask = mask;
+  f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha; f.gb = grad_beta;
   f.C = cfg->C; f.B = cfg->B; f.P = ba.P; f.wide = ba.wide; f.stateful = cfg->stateful;
   f.nA = int64_t(p.G) * p.ntiles;
   const int64_t nout = cfg->C * 3 * cfg->B;
-  const int64_t nblk = (f.wide ? ceil_div(nout, kThreads / 64) : ceil_div(nout, kThreads)) + 1;
+  const int64_t nblk = (f.wide ? ceil_div(nout, kThreads / 64) : ceil_div(nout, kThreads)) + 2;
   dendsn_finalize_kernel<<<dim3(unsigned(nblk)), dim3(kThreads), 0, stream>>>(f);
   e = hipGetLastError();
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("finalize launch: ") + hipGetErrorString(e));

@@ -1,18 +1,25 @@
 // Forward-kernel instantiations and dispatch for f32 storage.
+// V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite.
 #include "dendsn_kernels.h"
 
 namespace dendsn {
 
-hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G)), block(kThreads);
-#define DENDSN_CASE(BL_, L_)                                                        \
-  if (pl.BL == BL_ && pl.L == L_) {                                                 \
-    if (psi)                                                                        \
-      dendsn_fwd_kernel<float, BL_, L_, 1><<<grid, block, 0, stream>>>(fa);          \
-    else                                                                            \
-      dendsn_fwd_kernel<float, BL_, L_, 0><<<grid, block, 0, stream>>>(fa);          \
-    return hipGetLastError();                                                       \
+template <int BL, int L>
+static hipError_t launch_fwd_v(const dim3& grid, const FwdArgs& fa, int v, hipStream_t stream) {
+  switch (v) {
+    case 0: dendsn_fwd_kernel<float, BL, L, 0><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 1: dendsn_fwd_kernel<float, BL, L, 1><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 2: dendsn_fwd_kernel<float, BL, L, 2><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 3: dendsn_fwd_kernel<float, BL, L, 3><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
+#define DENDSN_CASE(BL_, L_) \
+  if (pl.BL == BL_ && pl.L == L_) return launch_fwd_v<BL_, L_>(grid, fa, v, stream);
   DENDSN_FAST_F32(DENDSN_CASE)
   DENDSN_GENERIC(DENDSN_CASE)
 #undef DENDSN_CASE

@@ -25,6 +25,11 @@ namespace dendsn {
 
 typedef uint16_t bf16_t;  // bf16 storage
 
+// Kernel variant V: bit 0 = Mexican-hat activation (else identity), bit 1 =
+// residual dendrite (Z also receives the mean synaptic input of the neuron).
+template <int V> constexpr bool kMH = (V & 1) != 0;
+template <int V> constexpr bool kRes = (V & 2) != 0;
+
 // -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.721347520444481703680f;
 constexpr float kLog2e = 1.442695040888963407360f;
@@ -258,6 +263,7 @@ struct Branches {
   float xi[BL];
   float rz[BL];  // 1 / zeta
   bool on[BL];   // mask bit
+  float rp;      // 1 / P, the residual term's weight of each compartment
 };
 
 template <int BL>
@@ -271,6 +277,7 @@ __device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int 
     br.xi[j] = a.xi ? a.xi[base + j] : 0.0f;
     br.rz[j] = a.zeta ? 1.0f / a.zeta[base + j] : 1.0f;
   }
+  br.rp = a.rP;
 }
 
 // ---------------------------------------------------------------------------
@@ -279,7 +286,7 @@ __device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int 
 // A gated-off branch keeps a zero state, so nothing it receives can reach the
 // soma or its gradients.
 // ---------------------------------------------------------------------------
-template <int BL, int L, int PSI>
+template <int BL, int L, int V>
 __device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv)[BL],
                                                const Branches<BL>& br, float alpha,
                                                float* efac = nullptr) {
@@ -291,7 +298,7 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv
     vd[j] = v;
     const float tt = (v - br.xi[j]) * br.rz[j];   // signed (Vd - xi)/zeta; u = |tt|
     float y;
-    if constexpr (PSI == 1) {
+    if constexpr (kMH<V>) {
       const float q = tt * tt;
       const float e = __builtin_amdgcn_exp2f(q * kNegHalfLog2e);
       if (efac) efac[j] = e;
@@ -299,7 +306,10 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv
     } else {
       y = fabsf(tt);
     }
-    part[j] = br.k[j] * y;
+    if constexpr (kRes<V>)
+      part[j] = fmaf(xv[j], br.rp, br.k[j] * y);  // every compartment feeds the residual
+    else
+      part[j] = br.k[j] * y;
   }
   return group_sum<L>(lane_sum<BL>(part));
 }
@@ -446,7 +456,7 @@ __device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, Fw
   st.s = false;
 }
 
-template <typename IO, int BL, int L, int PSI, int D>
+template <typename IO, int BL, int L, int V, int D>
 __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL>& br,
                                               float alpha, bool lead, int T, int Tp, int64_t item_neurons,
                                               const float (&buf)[D][BL], FwdLane<IO, BL>& st) {
@@ -454,7 +464,7 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = st.t + k;
-    const float z = dendrite_step<BL, L, PSI>(st.vd, buf[k], br, alpha);
+    const float z = dendrite_step<BL, L, V>(st.vd, buf[k], br, alpha);
     soma_step(st.h, st.s, z, a.beta, a.vth);
     if (t < T) {  // padded steps store nothing
       if (lead) {
@@ -481,9 +491,10 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
   }
 }
 
-template <typename IO, int BL, int L, int PSI>
+template <typename IO, int BL, int L, int V>
 __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   constexpr int D = 4;  // rows per chunk; two chunks in flight per lane
+  if (fa.s.beta_p) fa.s.beta = fa.s.beta_p[0];  // learnable (PLIF) decay
   const ScanArgs& a = fa.s;
   const Pos pos = locate<L>(a);
   if (!pos.active) return;  // whole L-lane groups leave together
@@ -511,9 +522,9 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
   for (int c = 0; c < nchunks; c += 2) {
     if (c + 1 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufB);
-    compute_chunk<IO, BL, L, PSI, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
     if (c + 2 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
-    if (c + 1 < nchunks) compute_chunk<IO, BL, L, PSI, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
+    if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
   }
 }
 
@@ -529,7 +540,8 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
 template <int BL>
 struct Accum {
   float k[BL], xi[BL], z[BL];
-  float a;
+  float a;   // g_alpha terms of this lane's branches
+  float b;   // g_beta terms of this lane's neuron (counted by its first lane only)
 };
 
 template <typename IO, int BL>
@@ -601,28 +613,30 @@ __device__ __forceinline__ void load_seg_start(const BwdArgs& ba, const LaneOff&
 // Registers a chunk's recompute leaves for its adjoint pass: the dendritic
 // state before and at each step, H at each step and, for the Mexican hat, the
 // exp(-u^2/2) factor of each step.
-template <int BL, int CS, int PSI>
+template <int BL, int CS, int V>
 struct Stash {
   float v[CS + 1][BL];
-  float e[PSI == 1 ? CS : 1][BL];
+  float e[kMH<V> ? CS : 1][BL];
   float h[CS];
+  float hd0;  // (1 - S) H before the chunk's first step: the decayed term beta multiplies
 };
 
 // Re-runs the chunk's forward steps exactly as the forward kernel did (the same
 // inline step function, so the same bits).
-template <int BL, int L, int PSI, int CS>
+template <int BL, int L, int V, int CS>
 __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branches<BL>& br, float alpha,
                                                 const float (&v0)[BL], float h0, bool s0,
-                                                const float (&x)[CS][BL], Stash<BL, CS, PSI>& st) {
+                                                const float (&x)[CS][BL], Stash<BL, CS, V>& st) {
 #pragma unroll
   for (int j = 0; j < BL; ++j) st.v[0][j] = v0[j];
+  st.hd0 = s0 ? 0.0f : h0;
   float h = h0;
   bool s = s0;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
 #pragma unroll
     for (int j = 0; j < BL; ++j) st.v[k + 1][j] = st.v[k][j];
-    const float z = dendrite_step<BL, L, PSI>(st.v[k + 1], x[k], br, alpha, PSI == 1 ? st.e[PSI == 1 ? k : 0] : nullptr);
+    const float z = dendrite_step<BL, L, V>(st.v[k + 1], x[k], br, alpha, kMH<V> ? st.e[kMH<V> ? k : 0] : nullptr);
     soma_step(h, s, z, a.beta, a.vth);
     st.h[k] = h;
   }
@@ -630,9 +644,9 @@ __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branche
 
 // The adjoint recurrences through one chunk, last step first; writes grad_x
 // and accumulates the parameter gradients.
-template <typename IO, int BL, int L, int PSI, int CS>
+template <typename IO, int BL, int L, int V, int CS>
 __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
-                                              float alpha, float beta_r, int c0, const Stash<BL, CS, PSI>& st,
+                                              float alpha, float beta_r, int c0, const Stash<BL, CS, V>& st,
                                               const float (&gs)[CS], const float (&gvr)[CS], BwdLane<IO, BL>& bl,
                                               Accum<BL>& acc) {
   const ScanArgs& a = ba.s;
@@ -646,14 +660,17 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
     const float dS = fmaf(-beta_r * hk, bl.dh_next, gs[k]);  // beta_r = 0: reset detached
     float dh = fmaf(sgv, dS, gvr[k]);
     dh = sk ? dh : fmaf(beta, bl.dh_next, dh);
+    // H[t] = beta (1 - S[t-1]) H[t-1] + Z[t]: learnable-beta (PLIF) gradient
+    const float hd = k > 0 ? (st.h[k > 0 ? k - 1 : 0] >= vth ? 0.0f : st.h[k > 0 ? k - 1 : 0]) : st.hd0;
+    acc.b = fmaf(dh, hd, acc.b);
     float gxo[BL];
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
       const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
       float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
-      if constexpr (PSI == 1) {
+      if constexpr (kMH<V>) {
         const float q = tt * tt;
-        const float e = st.e[PSI == 1 ? k : 0][j];
+        const float e = st.e[kMH<V> ? k : 0][j];
         y = (1.0f - q) * e;
         dps = tt * (q - 3.0f) * e;
       } else {
@@ -662,7 +679,7 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
       }
       const float r = (br.k[j] * dh) * dps * br.rz[j];
       bl.lam[j] = fmaf(alpha, bl.lam[j], r);
-      gxo[j] = bl.lam[j];
+      gxo[j] = kRes<V> ? fmaf(dh, br.rp, bl.lam[j]) : bl.lam[j];
       acc.k[j] = fmaf(dh, y, acc.k[j]);
       acc.xi[j] -= r;
       acc.z[j] = fmaf(-r, tt, acc.z[j]);
@@ -673,18 +690,18 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
   }
 }
 
-template <typename IO, int BL, int L, int PSI, int CS>
+template <typename IO, int BL, int L, int V, int CS>
 __device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
                                           float alpha, float beta_r, int c0, const float (&v0)[BL], float h0,
                                           bool s0, const ChunkIn<BL, CS>& in, BwdLane<IO, BL>& bl,
                                           Accum<BL>& acc) {
-  Stash<BL, CS, PSI> st;
-  recompute_chunk<BL, L, PSI, CS>(ba.s, br, alpha, v0, h0, s0, in.x, st);
-  reverse_chunk<IO, BL, L, PSI, CS>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
+  Stash<BL, CS, V> st;
+  recompute_chunk<BL, L, V, CS>(ba.s, br, alpha, v0, h0, s0, in.x, st);
+  reverse_chunk<IO, BL, L, V, CS>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
 }
 
 // Runs the forward from (vd, h, s) at step t_from up to (not including) t_to.
-template <typename IO, int BL, int L, int PSI>
+template <typename IO, int BL, int L, int V>
 __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, const Branches<BL>& br,
                                         float alpha, const IO* xbase, int t_from, int t_to, float (&vd)[BL],
                                         float& h, bool& s) {
@@ -692,13 +709,13 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
   for (int t = t_from; t < t_to; ++t) {
     float xv[BL];
     load_vec<BL>(at(xbase + int64_t(t) * rowX, lo.x), xv);
-    const float z = dendrite_step<BL, L, PSI>(vd, xv, br, alpha);
+    const float z = dendrite_step<BL, L, V>(vd, xv, br, alpha);
     soma_step(h, s, z, a.beta, a.vth);
   }
 }
 
 // Loads a chunk of CS steps and runs it (used for every chunk but a prefetched one).
-template <typename IO, int BL, int L, int PSI, int CS>
+template <typename IO, int BL, int L, int V, int CS>
 __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
                                                    float alpha, float beta_r, int t0, int c0, const SegStart<BL>& ss,
                                                    BwdLane<IO, BL>& bl, Accum<BL>& acc) {
@@ -709,8 +726,8 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
   for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
   float h = ss.h;
   bool s = ss.h >= ba.s.vth && t0 > 0;
-  advance<IO, BL, L, PSI>(ba.s, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-  bwd_chunk<IO, BL, L, PSI, CS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+  advance<IO, BL, L, V>(ba.s, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+  bwd_chunk<IO, BL, L, V, CS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
 }
 
 // Chunk plan of a segment [t0, t1): whole KS-step chunks from t0, then the
@@ -718,7 +735,7 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
 // from the last step backwards.  A neuron's first visited chunk is the top of
 // its last segment; it is a full KS chunk exactly when that segment's length
 // is a multiple of KS, and only then is it prefetched.
-template <typename IO, int BL, int L, int PSI, int KS>
+template <typename IO, int BL, int L, int V, int KS>
 __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff& lo, int64_t bt,
                                                 const Branches<BL>& br, float alpha, Accum<BL>& acc) {
   const ScanArgs& a = ba.s;
@@ -757,8 +774,8 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
       for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
       float h = ss.h;
       bool s = ss.h >= a.vth && t0 > 0;
-      advance<IO, BL, L, PSI>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-      bwd_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+      advance<IO, BL, L, V>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
+      bwd_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
     }
     // remainder pieces fill [t0, t0 + rem) with the largest on top and the
     // smallest at t0 (their re-advances then sum to the least); top one first
@@ -767,9 +784,9 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
     for (int cs = KS / 2; cs >= 1; cs /= 2) {
       if (rem & cs) {
         const int c0 = top - cs;
-        if (cs == 4) load_and_run_chunk<IO, BL, L, PSI, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
-        else if (cs == 2) load_and_run_chunk<IO, BL, L, PSI, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
-        else load_and_run_chunk<IO, BL, L, PSI, 1>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        if (cs == 4) load_and_run_chunk<IO, BL, L, V, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else if (cs == 2) load_and_run_chunk<IO, BL, L, V, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else load_and_run_chunk<IO, BL, L, V, 1>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
         top = c0;
       }
     }
@@ -781,7 +798,7 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
 // next neuron's rows are requested right after this neuron's recompute, when
 // the registers of its own rows are free again, so they stream in while the
 // adjoint pass runs.
-template <typename IO, int BL, int L, int PSI, int KS>
+template <typename IO, int BL, int L, int V, int KS>
 __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
                                                    float alpha, int64_t bt0, int nk, Accum<BL>& acc) {
   const ScanArgs& a = ba.s;
@@ -804,12 +821,12 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
     bl.dh_next = 0.0f;
 #pragma unroll
     for (int j = 0; j < BL; ++j) bl.lam[j] = 0.0f;
-    Stash<BL, KS, PSI> st;
-    recompute_chunk<BL, L, PSI, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
+    Stash<BL, KS, V> st;
+    recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
     ChunkIn<BL, KS> nxt;
     const int64_t n1 = n0 + step;
     if (i + 1 < nk) load_chunk_in<IO, BL, KS>(a, lo, x + n1 * a.B, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
-    reverse_chunk<IO, BL, L, PSI, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
+    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
     cur = nxt;
     n0 = n1;
   }
@@ -829,14 +846,21 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
   const ScanArgs& a = ba.s;
   __shared__ float red[kThreads * BL];
   __shared__ float reda[kThreads / 64];
+  __shared__ float redb[kThreads / 64];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int B = a.B;
 
-  float va = acc.a;
+  float va = acc.a, vb = acc.b;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) va += __shfl_xor(va, off);
-  if (lane == 0) reda[wave] = va;
+  for (int off = 32; off >= 1; off >>= 1) {
+    va += __shfl_xor(va, off);
+    vb += __shfl_xor(vb, off);
+  }
+  if (lane == 0) {
+    reda[wave] = va;
+    redb[wave] = vb;
+  }
 
   if (a.mode == kSpatial) {
     // One channel per block: sum lanes of equal sub within the wave, then waves.
@@ -884,17 +908,22 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
     }
   }
   __syncthreads();
-  if (tid == 0) ba.wsA[int64_t(pos.g) * a.ntiles + pos.tile] = (reda[0] + reda[1]) + (reda[2] + reda[3]);
+  if (tid == 0) {
+    ba.wsA[int64_t(pos.g) * a.ntiles + pos.tile] = (reda[0] + reda[1]) + (reda[2] + reda[3]);
+    ba.wsB[int64_t(pos.g) * a.ntiles + pos.tile] = (redb[0] + redb[1]) + (redb[2] + redb[3]);
+  }
 }
 
-template <typename IO, int BL, int L, int PSI, int KS>
+template <typename IO, int BL, int L, int V, int KS>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * KS <= 8 ? 4 : (BL * KS <= 16 ? 3 : 2)))) dendsn_bwd_kernel(BwdArgs ba) {
+  if (ba.s.beta_p) ba.s.beta = ba.s.beta_p[0];  // learnable (PLIF) decay
   const ScanArgs& a = ba.s;
   const Pos pos = locate<L>(a);
   Accum<BL> acc;
 #pragma unroll
   for (int j = 0; j < BL; ++j) acc.k[j] = acc.xi[j] = acc.z[j] = 0.0f;
   acc.a = 0.0f;
+  acc.b = 0.0f;
   if (pos.active) {
     Branches<BL> br;
     load_branches<BL>(a, pos.c, pos.sub, br);
@@ -906,15 +935,16 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     bool single = false;
     if constexpr (KS == 4) {
       if (T == KS) {
-        single_chunk_items<IO, BL, L, PSI, KS>(ba, lo, br, alpha, bt0, nk, acc);
+        single_chunk_items<IO, BL, L, V, KS>(ba, lo, br, alpha, bt0, nk, acc);
         single = true;
       }
     }
     if (!single) {
       for (int i = 0; i < nk; ++i)
-        backward_neuron<IO, BL, L, PSI, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
+        backward_neuron<IO, BL, L, V, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
     }
   }
+  if (pos.sub != 0) acc.b = 0.0f;  // the soma runs in every lane of a neuron: count it once
   // every thread of the block reaches this one call (it holds block barriers)
   reduce_partials<BL, L>(ba, pos, acc);
 }

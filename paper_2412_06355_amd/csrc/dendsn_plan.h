@@ -40,9 +40,11 @@ struct ScanArgs {
   const float* xi;      // NULL: 0
   const float* zeta;    // NULL: 1
   const uint8_t* mask;  // NULL: all branches kept
+  const float* beta_p;  // learnable somatic decay on the device, or NULL: beta
   int64_t T, N, C, S, M, batch;  // M = C * S positions per sample
   int32_t B, K, nck;
   float beta, vth;
+  float rP;             // 1 / P (residual dendrite)
   int32_t mode, ways, pb, tpc, cpt, bpg;
   int64_t ntiles;
 };
@@ -62,6 +64,7 @@ struct BwdArgs {
   void* gx;
   float* wsP;       // partial sums of (g_kappa, g_xi, g_zeta): P slots per output, see partial_index
   float* wsA;       // [G][ntiles] partial sums of g_alpha
+  float* wsB;       // [G][ntiles] partial sums of g_beta
   int64_t P;        // partial slots per output: G * tpc
   int32_t wide;     // 1: output-major layout (P > kNarrowSlots)
   int32_t detach;
@@ -72,6 +75,8 @@ struct BwdArgs {
 struct FinArgs {
   const float* wsP;
   const float* wsA;
+  const float* wsB;
+  float* gb;
   const uint8_t* mask;
   float* gk;
   float* gxi;
@@ -88,9 +93,6 @@ constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread p
 // for every mapping, and 8 steps too when a lane holds at most 4 branches.
 #define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
 #define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
-// Backward-only splits with 2 branches per lane (same branch-sum tree as the
-// forward's 4 or 8 per lane, so the recompute stays bit-identical).
-#define DENDSN_BWD_HALF(X) X(2, 2) X(2, 4) X(2, 8) X(2, 16)
 #define DENDSN_GENERIC(X) X(1, 1) X(2, 1) X(3, 1) X(5, 1) X(6, 1) X(7, 1) X(5, 2) X(6, 2) X(7, 2)
 #define DENDSN_GENERIC_KS 4
 

@@ -63,6 +63,11 @@ class Case:
     alpha: float
     gV: np.ndarray | None = None
     name: str = ""
+    beta_dev: float | None = None    # learnable somatic decay (PLIF) passed on the device
+
+    @property
+    def beta(self) -> float:
+        return self.cfg.beta if self.beta_dev is None else self.beta_dev
 
 
 @dataclass
@@ -76,7 +81,7 @@ class Report:
 
 
 def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True, mask_rho=None,
-              with_gv=False, name=""):
+              with_gv=False, name="", beta_dev=None):
     """Seeded inputs for a config (numpy PCG64).  bf16 storage is emulated by
     rounding the float32 draws to bf16 (round to nearest even) with torch."""
     import torch
@@ -96,7 +101,8 @@ def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True,
         xi = zeta = None
     mask = (rng.random((C, B)) < mask_rho).astype(np.uint8) if mask_rho is not None else None
     gV = rng.normal(size=(T, N)).astype(np.float32) if with_gv else None
-    return Case(cfg=cfg, X=X, gS=gS, kappa=kappa, xi=xi, zeta=zeta, mask=mask, alpha=alpha, gV=gV, name=name)
+    return Case(cfg=cfg, X=X, gS=gS, kappa=kappa, xi=xi, zeta=zeta, mask=mask, alpha=alpha, gV=gV, name=name,
+                beta_dev=beta_dev)
 
 
 # ---------------------------------------------------------------------------
@@ -111,6 +117,8 @@ def to_device(case: Case, device):
     return dict(
         x=t(case.X, io), gS=t(case.gS, io), gV=t(case.gV),
         alpha=torch.tensor([case.alpha], dtype=torch.float32, device=device),
+        beta=None if case.beta_dev is None else torch.tensor([case.beta_dev], dtype=torch.float32,
+                                                             device=device),
         kappa=t(case.kappa), xi=t(case.xi), zeta=t(case.zeta),
         mask=None if case.mask is None else torch.from_numpy(case.mask).to(device),
     )
@@ -125,13 +133,13 @@ def run_gpu(case: Case, device, dev=None, want_v_soma=True):
     announce(f"case {case.name or '?'}: {case.cfg}")
     d = dev if dev is not None else to_device(case, device)
     spikes, v_soma, ckpt = dendsn.forward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"],
-                                          d["mask"], want_v_soma=want_v_soma)
+                                          d["mask"], beta=d["beta"], want_v_soma=want_v_soma)
     g = dendsn.backward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"], ckpt,
-                        d["gS"], d["gV"])
+                        d["gS"], d["gV"], beta=d["beta"])
     torch.cuda.synchronize(device)
     f = lambda t: None if t is None else t.float().cpu().numpy().astype(np.float64)
     return dict(S=f(spikes), H=f(v_soma), gX=f(g["grad_x"]), g_alpha=float(g["grad_alpha"].item()),
-                g_kappa=f(g["grad_kappa"]), g_xi=f(g["grad_xi"]), g_zeta=f(g["grad_zeta"]),
+                g_beta=float(g["grad_beta"].item()), g_kappa=f(g["grad_kappa"]), g_xi=f(g["grad_xi"]), g_zeta=f(g["grad_zeta"]),
                 raw=dict(spikes=spikes, v_soma=v_soma, grads=g))
 
 
@@ -141,9 +149,9 @@ def run_gpu(case: Case, device, dev=None, want_v_soma=True):
 def run_oracle(case: Case, force=None):
     cfg = case.cfg
     rec = oracle.forward(
-        case.X.astype(np.float64), alpha=case.alpha if cfg.stateful else 0.0, beta=cfg.beta, v_th=cfg.v_th,
+        case.X.astype(np.float64), alpha=case.alpha if cfg.stateful else 0.0, beta=case.beta, v_th=cfg.v_th,
         kappa=case.kappa, xi=case.xi, zeta=case.zeta, mask=case.mask, C=cfg.C, S=cfg.S,
-        psi_kind=cfg.psi, stateful=cfg.stateful, force=force)
+        psi_kind=cfg.psi, stateful=cfg.stateful, residual=cfg.residual, force=force)
     return rec
 
 
@@ -183,10 +191,11 @@ def cfg_vth(case):
     return case.cfg.v_th
 
 
-def horizon_growth(cfg, alpha: float) -> float:
+def horizon_growth(cfg, alpha: float, beta: float | None = None) -> float:
     """Elementwise tolerance factor g = max(1, h(beta) h(alpha) / 4)."""
     h = lambda x: min(float(cfg.T), 1.0 / (1.0 - x))
-    return max(1.0, h(cfg.beta) * (h(alpha) if cfg.stateful else 1.0) / 4.0)
+    b = cfg.beta if beta is None else beta
+    return max(1.0, h(b) * (h(alpha) if cfg.stateful else 1.0) / 4.0)
 
 
 def close_normwise(name, g, o, rtol, report: Report):
@@ -233,7 +242,7 @@ def compare(case: Case, gpu: dict) -> Report:
     assert np.array_equal(gpu["S"], rec["S"])
     assert set(np.unique(gpu["S"])).issubset({0.0, 1.0})
     og = oracle_grads(case, rec)
-    gr = horizon_growth(cfg, case.alpha)
+    gr = horizon_growth(cfg, case.alpha, case.beta)
     if gpu["H"] is not None:
         close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, gr, rep)
     rt_io = RTOL_BF16 if cfg.io == "bf16" else RTOL_F32
@@ -242,10 +251,14 @@ def compare(case: Case, gpu: dict) -> Report:
         close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, gr, rep)
     close_summed("g_alpha", gpu["g_alpha"], og["g_alpha"] if cfg.stateful else 0.0,
                  og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, gr, rep)
+    close_summed("g_beta", gpu["g_beta"], og["g_beta"], og["abs_beta"], RTOL_F32, gr, rep)
     if case.mask is not None:
         off = case.mask == 0
         for k in ("g_kappa", "g_xi", "g_zeta"):
             assert np.all(gpu[k][off] == 0.0), k
-        cidx = (np.arange(cfg.N) // cfg.S) % cfg.C
-        assert np.all(gpu["gX"][:, off[cidx]] == 0.0)
+        if not cfg.residual:
+            # a gated-off branch feeds nothing to the soma; with the residual
+            # dendrite its input still reaches the soma through the mean
+            cidx = (np.arange(cfg.N) // cfg.S) % cfg.C
+            assert np.all(gpu["gX"][:, off[cidx]] == 0.0)
     return rep

@@ -29,7 +29,7 @@ def header_functions():
 
 def base_cfg(**kw):
     c = dict(T=4, batch=2, C=256, S=1, B=4, comps_per_branch=1, stateful=1, detach_reset=0,
-             ckpt_every=4, io=0, psi=1, sg=1, sg_scale=4.0, beta=0.5, v_th=1.0, batch_groups=0)
+             ckpt_every=4, io=0, psi=1, sg=1, sg_scale=4.0, beta=0.5, v_th=1.0, batch_groups=0, residual=0)
     c.update(kw)
     return dendsn_cfg(**c)
 
@@ -50,16 +50,17 @@ GOOD = 0x10000  # 64 KiB-aligned fake device address
 
 
 def fwd(lib, cfg, x=GOOD, alpha=GOOD + 0x100, kappa=GOOD + 0x200, xi=None, zeta=None, mask=None,
-        spikes=GOOD + 0x300, v_soma=None, ckpt=None):
+        spikes=GOOD + 0x300, v_soma=None, ckpt=None, beta=None):
     p = lambda v: None if v is None else fake(v)
-    return lib.dendsn_forward(ctypes.byref(cfg), p(x), p(alpha), p(kappa), p(xi), p(zeta), p(mask),
+    return lib.dendsn_forward(ctypes.byref(cfg), p(x), p(alpha), p(beta), p(kappa), p(xi), p(zeta), p(mask),
                               p(spikes), p(v_soma), p(ckpt), None)
 
 
-def bwd(lib, cfg, ckpt=None, ws=GOOD + 0x1000, ws_bytes=1 << 40, x=GOOD, gx=GOOD + 0x400, gs=GOOD + 0x500):
+def bwd(lib, cfg, ckpt=None, ws=GOOD + 0x1000, ws_bytes=1 << 40, x=GOOD, gx=GOOD + 0x400, gs=GOOD + 0x500,
+        beta=None, grad_beta=None):
     p = lambda v: None if v is None else fake(v)
-    return lib.dendsn_backward(ctypes.byref(cfg), p(x), p(GOOD + 0x100), p(GOOD + 0x200), None, None, None,
-                               p(ckpt), p(gs), None, p(gx), None, None, None, None, p(ws),
+    return lib.dendsn_backward(ctypes.byref(cfg), p(x), p(GOOD + 0x100), p(beta), p(GOOD + 0x200), None, None,
+                               None, p(ckpt), p(gs), None, p(gx), None, p(grad_beta), None, None, None, p(ws),
                                ctypes.c_size_t(ws_bytes), None)
 
 
@@ -100,6 +101,7 @@ def test_workspace_bytes_positive_and_grows_with_groups(lib):
     (dict(sg_scale=0.0), E_INVALID), (dict(sg_scale=float("nan")), E_INVALID),
     (dict(beta=float("inf")), E_INVALID), (dict(v_th=float("nan")), E_INVALID),
     (dict(batch_groups=-1), E_INVALID), (dict(batch=1 << 40, C=1 << 10), E_INVALID),
+    (dict(residual=2), E_INVALID), (dict(residual=-1), E_INVALID),
 ])
 def test_bad_cfg_rejected_everywhere(lib, kw, code):
     cfg = base_cfg(**kw)
@@ -115,7 +117,8 @@ def test_bad_cfg_rejected_everywhere(lib, kw, code):
 def test_null_cfg(lib):
     out = ctypes.c_size_t(0)
     assert lib.dendsn_ckpt_bytes(None, ctypes.byref(out)) == E_INVALID
-    assert lib.dendsn_forward(None, *([None] * 10)) == E_INVALID
+    assert lib.dendsn_forward(None, *([None] * 11)) == E_INVALID
+    assert lib.dendsn_backward(None, *([None] * 17), ctypes.c_size_t(0), None) == E_INVALID
 
 
 def test_sigmoid_scale_ignored_for_atan(lib):
@@ -132,6 +135,9 @@ def test_forward_argument_checks(lib):
     assert fwd(lib, cfg, alpha=None) == E_INVALID          # stateful needs alpha
     assert fwd(lib, cfg, x=GOOD + 4) == E_INVALID           # x must be 16-byte aligned
     assert fwd(lib, cfg, spikes=GOOD + 2) == E_INVALID      # fp32 spikes misaligned
+    assert fwd(lib, cfg, beta=GOOD + 2) == E_INVALID        # device beta misaligned
+    assert bwd(lib, cfg, beta=GOOD + 2) == E_INVALID
+    assert bwd(lib, cfg, grad_beta=GOOD + 0x702) == E_INVALID
     assert fwd(lib, cfg, ckpt=GOOD + 8) == E_INVALID
     assert "align" in dendsn.dendsn_last_error()
 

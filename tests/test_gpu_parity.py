@@ -67,17 +67,58 @@ SHAPES = [
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}{}K{}".format(*s))
-@pytest.mark.parametrize("variant", ["mh-sig-mask", "id-atan-stateless", "mh-atan-detach"])
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "id-atan-stateless", "mh-atan-detach",
+                                     "res-mh-sig-mask-plif", "res-id-atan-stateless"])
 def test_shapes(gpu_device, shape, variant):
     T, batch, C, S, B, io, K = shape
-    psi = "mexhat" if variant.startswith("mh") else "identity"
+    psi = "identity" if "-id-" in f"-{variant}-" else "mexhat"
     sg = "sigmoid" if "sig" in variant else "atan"
     c = cfg(T=T, batch=batch, C=C, S=S, B=B, io=io, ckpt_every=K, psi=psi, sg=sg,
-            stateful="stateless" not in variant, detach_reset="detach" in variant, beta=0.7)
+            stateful="stateless" not in variant, detach_reset="detach" in variant, beta=0.7,
+            residual=variant.startswith("res"))
     seed = zlib.crc32(repr((shape, variant)).encode()) % 1000
     case = make_case(c, seed=seed, x_std=1.2, alpha=0.6,
-                     mask_rho=0.5 if "mask" in variant else None, name=f"{shape}/{variant}")
+                     mask_rho=0.5 if "mask" in variant else None, name=f"{shape}/{variant}",
+                     beta_dev=0.8 if "plif" in variant else None)
     compare(case, run_gpu(case, gpu_device))
+
+
+# --- residual dendrite (ResStateful / ResStateless) and the PLIF soma ---
+@pytest.mark.parametrize("stateful", [True, False])
+@pytest.mark.parametrize("plif", [False, True])
+@pytest.mark.parametrize("detach", [False, True])
+def test_tiny_residual_and_plif(gpu_device, stateful, plif, detach):
+    c = cfg(stateful=stateful, residual=True, detach_reset=detach)
+    case = make_case(c, seed=3, with_gv=True, name=f"tiny/res/stateful={stateful}/plif={plif}/detach={detach}",
+                     beta_dev=0.65 if plif else None)
+    rep = compare(case, run_gpu(case, gpu_device))
+    print(rep)
+
+
+def test_device_beta_overrides_cfg_beta(gpu_device):
+    """A device beta is the decay the scan uses: bit-identical to the same value in cfg."""
+    import torch
+
+    base = cfg(T=9, batch=3, C=40, S=17, B=8, ckpt_every=4)
+    case = make_case(base.with_(beta=0.1), seed=21, mask_rho=0.6, name="device-beta", beta_dev=0.85)
+    d = to_device(case, gpu_device)
+    a = run_gpu(case, gpu_device, dev=d)
+    compare(case, a)
+    case.cfg, case.beta_dev = base.with_(beta=0.85), None
+    d["beta"] = None
+    b = run_gpu(case, gpu_device, dev=d)
+    assert torch.equal(a["raw"]["spikes"], b["raw"]["spikes"])
+    for k in a["raw"]["grads"]:
+        assert torch.equal(_bits(a["raw"]["grads"][k]), _bits(b["raw"]["grads"][k])), k
+
+
+def test_dbg_per_task_dense_strengths(gpu_device):
+    """DBG_e: each task keeps its own dense branch strengths kappa_q next to its
+    mask m_q; a call for task q passes kappa_q and m_q."""
+    c = cfg(T=4, batch=3, C=96, S=1, B=16, residual=False)
+    for q in range(3):
+        case = make_case(c, seed=40 + q, mask_rho=0.5, name=f"dbg-e/task{q}")
+        compare(case, run_gpu(case, gpu_device))
 
 
 # --- the benchmark layer shapes with the batch cut down (every other size kept) ---
@@ -86,6 +127,9 @@ REDUCED = {
     "imagenet_stem": dict(T=4, batch=1, C=64, S=12544, B=4, io="bf16"),
     "long_horizon": dict(T=64, batch=2, C=4096, S=1, B=16, x_mean=0.1, alpha=0.8, beta=0.9, ckpt_every=8),
     "dbg": dict(T=4, batch=2, C=8192, S=1, B=32, mask_rho=0.5),
+    "long_horizon_res_plif": dict(T=64, batch=2, C=4096, S=1, B=16, x_mean=0.1, alpha=0.8, beta=0.9,
+                                  ckpt_every=8, residual=True, beta_dev=0.9),
+    "cifar_res": dict(T=4, batch=2, C=128, S=1024, B=8, x_std=0.5, residual=True),
 }
 
 
@@ -94,9 +138,10 @@ def test_reduced_workloads(gpu_device, name):
     kw = dict(REDUCED[name])
     x_mean, x_std = kw.pop("x_mean", 0.0), kw.pop("x_std", 1.0)
     alpha, rho = kw.pop("alpha", 0.5), kw.pop("mask_rho", None)
+    beta_dev = kw.pop("beta_dev", None)
     c = cfg(**kw)
     case = make_case(c, seed=7, x_mean=x_mean, x_std=x_std, alpha=alpha, random_affine=False,
-                     mask_rho=rho, name=f"reduced/{name}")
+                     mask_rho=rho, name=f"reduced/{name}", beta_dev=beta_dev)
     rep = compare(case, run_gpu(case, gpu_device))
     print(name, rep)
 
