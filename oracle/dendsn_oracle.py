@@ -6,17 +6,21 @@ benchmark do.  It shares no code, constants or helpers with the HIP library.
 
 Every array is float64.  Shapes follow the layer form of the paper (Methods,
 "Dendritic spiking neural networks"): the synaptic input of one layer is
-``X[t, n, b]`` with T time steps, N = batch * C * S neurons ordered
-``(batch, channel, spatial)`` and one compartment per branch (P = B), so branch
-b of neuron n receives compartment b.  Neurons of one channel share the
-parameters xi, zeta, kappa (and the branch-gating mask); alpha is shared by the
-whole layer.
+``X[t, n, i]`` with T time steps, N = batch * C * S neurons ordered
+``(batch, channel, spatial)`` and P = B k compartments, k per branch (constraint
+(1): every branch holds P/B compartments).  Compartment i lies on branch
+b = i // k, i.e. the wiring matrix Gamma groups consecutive compartments
+(Gamma[b, i] = 1 iff b k <= i < (b + 1) k); with k = 1 compartment b is branch b.
+Neurons of one channel share the parameters (constraint (3)): the translation
+xi per compartment ``[C, P]``, the dilation zeta, the strength kappa and the
+branch-gating mask per branch ``[C, B]``; alpha is shared by the whole layer.
 
 Forward recurrences, in the paper's order (Methods, "Dendritic spiking neuron"):
 
-  Eq. (methods-compartment)         Vd_b[t] = alpha * Vd_b[t-1] + X_b[t],  Vd[0] = 0
-                                    (Stateless Dendrite variant: Vd_b[t] = X_b[t])
-  Eq. (methods-branch-aggregation)  u_b[t]  = |Vd_b[t] - xi_b| / zeta_b     (one compartment per branch)
+  Eq. (methods-compartment)         Vd_i[t] = alpha * Vd_i[t-1] + X_i[t],  Vd[0] = 0
+                                    (Stateless Dendrite variant: Vd_i[t] = X_i[t])
+  Eq. (methods-branch-aggregation)  d_i[t]  = Vd_i[t] - xi_i
+                                    u_b[t]  = sqrt(sum_{i in C_b} d_i[t]^2) / zeta_b
                                     Y_b[t]  = psi(u_b[t])
   Eq. (methods-mexican-hat)         psi(x)  = (1 - x^2) exp(-x^2 / 2)   ("MH"), or psi(x) = x ("Identity")
   Eq. (methods-soma-input)          Z[t]    = sum_b kappa*_b Y_b[t]
@@ -37,11 +41,14 @@ are the chain rule applied to the forward recurrences above, in reverse time:
   dS[t]   = gS[t] - beta H[t] dH[t+1]                 (second term dropped when the reset is detached)
   dH[t]   = gV[t] + sg(H[t] - v_th) dS[t] + beta (1 - S[t]) dH[t+1]
   g_beta += dH[t] (1 - S[t-1]) H[t-1]                 (PLIF soma: beta learnable)
-  g_u     = kappa*_b dH[t] psi'(u_b[t])
-  r_b[t]  = g_u sgn(Vd_b[t] - xi_b) / zeta_b          (sgn(0) = 0: the L2 norm's subgradient at 0)
-  lam_b[t]= r_b[t] + alpha lam_b[t+1]                 (Stateless: lam = r)
+  g_u_b   = kappa*_b dH[t] psi'(u_b[t])
+  r_i[t]  = g_u_b d_i[t] / (zeta_b ||d_{C_b}[t]||)    (d/dVd_i of u_b; the L2 norm's subgradient
+                                                       at 0 is taken as 0, which for k = 1 is
+                                                       r = g_u sgn(d) / zeta with sgn(0) = 0)
+  lam_i[t]= r_i[t] + alpha lam_i[t+1]                 (Stateless: lam = r)
   gX      = lam (+ dH / P with the residual term);
-  g_kappa += m dH Y;  g_xi += -r;  g_zeta += -g_u u / zeta;  g_alpha += lam_b[t] Vd_b[t-1]
+  g_kappa_b += m dH Y_b;  g_xi_i += -r_i;  g_zeta_b += -g_u_b u_b / zeta_b;
+  g_alpha   += sum_i lam_i[t] Vd_i[t-1]
 
 The backward consumes the recorded spikes S rather than re-deciding Theta, so
 that the oracle's gradient is exactly the gradient of the forward whose spikes
@@ -115,26 +122,29 @@ def surrogate_grad(x: np.ndarray, kind: str, scale: float = 4.0) -> np.ndarray:
 # constraint (3): per-channel parameters shared over spatial positions).
 # --------------------------------------------------------------------------
 def _per_neuron(p: np.ndarray, batch: int, C: int, S: int) -> np.ndarray:
-    """Expand a [C, B] per-channel table to [N, B] with N ordered (batch, C, S)."""
-    B = p.shape[1]
-    return np.broadcast_to(p[None, :, None, :], (batch, C, S, B)).reshape(batch * C * S, B)
+    """Expand a [C, W] per-channel table to [N, W] with N ordered (batch, C, S)."""
+    W = p.shape[1]
+    return np.broadcast_to(p[None, :, None, :], (batch, C, S, W)).reshape(batch * C * S, W)
 
 
 def _channel_sum(a: np.ndarray, batch: int, C: int, S: int) -> np.ndarray:
-    """Sum a [T, N, B] array over time, batch and spatial positions -> [C, B]."""
-    T, N, B = a.shape
-    return a.reshape(T, batch, C, S, B).sum(axis=(0, 1, 3))
+    """Sum a [T, N, W] array over time, batch and spatial positions -> [C, W]."""
+    T, N, W = a.shape
+    return a.reshape(T, batch, C, S, W).sum(axis=(0, 1, 3))
 
 
-def _check_shapes(X, kappa, C, S):
+def _check_shapes(X, kappa, C, S, k):
     if X.ndim != 3:
-        raise ValueError("X must be [T, N, B]")
-    T, N, B = X.shape
+        raise ValueError("X must be [T, N, P]")
+    T, N, P = X.shape
     if N % (C * S) != 0:
         raise ValueError("N must be batch * C * S")
+    if k < 1 or P % k != 0:
+        raise ValueError("P must be a multiple of the compartments per branch k")
+    B = P // k
     if kappa.shape != (C, B):
         raise ValueError("kappa must be [C, B]")
-    return T, N, B, N // (C * S)
+    return T, N, P, B, N // (C * S)
 
 
 # --------------------------------------------------------------------------
@@ -155,22 +165,27 @@ def forward(
     psi_kind: str = PSI_MEXHAT,
     stateful: bool = True,
     residual: bool = False,
+    comps_per_branch: int = 1,
     force: np.ndarray | None = None,
 ) -> dict:
     """Run the DendSN layer forward over all T steps.
 
-    X: [T, N, B]; kappa, xi, zeta: [C, B] (xi None -> 0, zeta None -> 1);
-    mask: [C, B] of {0, 1} or None (all ones).
+    X: [T, N, P] with P = B k, k = comps_per_branch; kappa, zeta: [C, B];
+    xi: [C, P] (xi None -> 0, zeta None -> 1); mask: [C, B] of {0, 1} or None
+    (all ones).
     force: optional [T, N] int array; entries 0 or 1 override the spike decision
     at that step (used to impose a decision taken elsewhere), -1 leaves it free.
 
-    Returns a record with Vd [T+1, N, B] (Vd[0] = 0), u, Y [T, N, B],
-    Z, H, S [T, N] and the inputs needed by ``backward``.
+    Returns a record with Vd [T+1, N, P] (Vd[0] = 0), d [T, N, P], the branch
+    norms, u and Y [T, N, B], Z, H, S [T, N] and the inputs ``backward`` needs.
     """
     X = np.asarray(X, dtype=np.float64)
     kappa = np.asarray(kappa, dtype=np.float64)
-    T, N, B, batch = _check_shapes(X, kappa, C, S)
-    xi = np.zeros((C, B)) if xi is None else np.asarray(xi, dtype=np.float64)
+    k = int(comps_per_branch)
+    T, N, P, B, batch = _check_shapes(X, kappa, C, S, k)
+    xi = np.zeros((C, P)) if xi is None else np.asarray(xi, dtype=np.float64)
+    if xi.shape != (C, P):
+        raise ValueError("xi must be [C, P]: one translation per compartment")
     zeta = np.ones((C, B)) if zeta is None else np.asarray(zeta, dtype=np.float64)
     m = np.ones((C, B)) if mask is None else (np.asarray(mask) != 0).astype(np.float64)
     if np.any(zeta <= 0):
@@ -185,8 +200,9 @@ def forward(
     kstar_n = _per_neuron(kappa * m, batch, C, S)
     m_n = _per_neuron(m, batch, C, S)
 
-    Vd = np.zeros((T + 1, N, B))
-    d = np.zeros((T, N, B))
+    Vd = np.zeros((T + 1, N, P))
+    d = np.zeros((T, N, P))
+    nrm = np.zeros((T, N, B))
     u = np.zeros((T, N, B))
     Y = np.zeros((T, N, B))
     Z = np.zeros((T, N))
@@ -197,9 +213,11 @@ def forward(
     for t in range(T):
         # Eq. (methods-compartment), or the Stateless Dendrite variant.
         Vd[t + 1] = alpha * Vd[t] + X[t] if stateful else X[t]
-        # Eq. (methods-branch-aggregation) with one compartment per branch.
+        # Eq. (methods-branch-aggregation): the L2 norm over the branch's k
+        # compartments (consecutive compartments share a branch), dilated by zeta_b.
         d[t] = Vd[t + 1] - xi_n
-        u[t] = np.abs(d[t]) / zeta_n
+        nrm[t] = np.sqrt((d[t] * d[t]).reshape(N, B, k).sum(axis=2))
+        u[t] = nrm[t] / zeta_n
         Y[t] = psi(u[t], psi_kind)
         # Eq. (methods-soma-input) with the gated strengths of Eq. (methods-dbg-mask).
         # A gated-off branch contributes nothing, whatever its Y.
@@ -207,7 +225,7 @@ def forward(
         if residual:
             # Eq. (methods-residual): the mean synaptic input of the P compartments
             # (gating scales branch strengths only, so every compartment takes part).
-            Z[t] = Z[t] + X[t].mean(axis=1)
+            Z[t] = Z[t] + X[t].sum(axis=1) / P
         # Eq. (methods-lif-reset-charge) and Eq. (methods-lif-fire).
         H[t] = beta * (1.0 - s_prev) * h_prev + Z[t]
         s = (H[t] - v_th >= 0.0).astype(np.float64)
@@ -218,7 +236,7 @@ def forward(
         h_prev, s_prev = H[t], s
 
     return dict(
-        X=X, Vd=Vd, d=d, u=u, Y=Y, Z=Z, H=H, S=Sp,
+        X=X, Vd=Vd, d=d, nrm=nrm, u=u, Y=Y, Z=Z, H=H, S=Sp, k=k,
         alpha=float(alpha), beta=float(beta), v_th=float(v_th),
         kappa=kappa, xi=xi, zeta=zeta, m=m, C=C, S_sp=S, batch=batch,
         psi_kind=psi_kind, stateful=bool(stateful), residual=bool(residual),
@@ -244,6 +262,8 @@ def backward(
     gradient's rounding error is judged.
     """
     T, N, B = rec["Y"].shape
+    k = rec["k"]
+    P = B * k
     C, S, batch = rec["C"], rec["S_sp"], rec["batch"]
     alpha, beta, v_th = rec["alpha"], rec["beta"], rec["v_th"]
     stateful = rec["stateful"]
@@ -254,16 +274,17 @@ def backward(
     kstar_n = _per_neuron(rec["kappa"] * rec["m"], batch, C, S)
     zeta_n = _per_neuron(rec["zeta"], batch, C, S)
     H, Sp, u, d, Y, Vd = rec["H"], rec["S"], rec["u"], rec["d"], rec["Y"], rec["Vd"]
+    nrm = rec["nrm"]
 
     dH = np.zeros((T, N))
-    gX = np.zeros((T, N, B))
+    gX = np.zeros((T, N, P))
     t_beta = np.zeros((T, N))
     t_kappa = np.zeros((T, N, B))
-    t_xi = np.zeros((T, N, B))
+    t_xi = np.zeros((T, N, P))
     t_zeta = np.zeros((T, N, B))
-    t_alpha = np.zeros((T, N, B))
+    t_alpha = np.zeros((T, N, P))
     dH_next = np.zeros(N)
-    lam_next = np.zeros((N, B))
+    lam_next = np.zeros((N, P))
     sg_all = surrogate_grad(H - v_th, sg_kind, sg_scale)
     for t in range(T - 1, -1, -1):
         # Somatic adjoint: S[t] feeds H[t+1] through the reset factor (1 - S[t]),
@@ -272,9 +293,14 @@ def backward(
         dH[t] = gV[t] + sg_all[t] * dS + beta * (1.0 - Sp[t]) * dH_next
         # Z[t] enters H[t] with unit weight, so dZ[t] = dH[t].
         g_u = kstar_n * dH[t][:, None] * dpsi(u[t], rec["psi_kind"])
-        r = np.where(m_n != 0, g_u * np.sign(d[t]) / zeta_n, 0.0)
+        # du_b/dVd_i = (d_i / ||d_b||) / zeta_b for i on branch b (for k = 1 the unit
+        # direction d / |d| is sgn(d) exactly); 0 where the norm vanishes and on
+        # gated-off branches (nothing of theirs reaches the soma).
+        live = np.repeat((m_n != 0) & (nrm[t] > 0.0), k, axis=1)                    # [N, P]
+        unit = np.where(live, d[t] / np.where(live, np.repeat(nrm[t], k, axis=1), 1.0), 0.0)
+        r = np.where(live, np.repeat(g_u, k, axis=1) * unit / np.repeat(zeta_n, k, axis=1), 0.0)
         lam = r + alpha * lam_next if stateful else r
-        gX[t] = lam + dH[t][:, None] / B if rec["residual"] else lam   # B compartments: P = B
+        gX[t] = lam + dH[t][:, None] / P if rec["residual"] else lam
         # H[t] = beta (1 - S[t-1]) H[t-1] + Z[t]: the PLIF soma's beta gradient
         if t > 0:
             t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]

@@ -18,19 +18,29 @@ MUTANTS = {
     "beta dropped from the leak": ("H[t] = beta * (1.0 - s_prev) * h_prev", "H[t] = (1.0 - s_prev) * h_prev"),
     "reset dropped": ("H[t] = beta * (1.0 - s_prev) * h_prev", "H[t] = beta * h_prev"),
     "atan surrogate missing pi": ("1.0 / (1.0 + (np.pi * x) ** 2)", "1.0 / (1.0 + (x) ** 2)"),
-    "zeta multiplies instead of divides": ("u[t] = np.abs(d[t]) / zeta_n", "u[t] = np.abs(d[t]) * zeta_n"),
+    "zeta multiplies instead of divides": ("u[t] = nrm[t] / zeta_n", "u[t] = nrm[t] * zeta_n"),
     "channel gather transposed (S, C order)": (
-        "np.broadcast_to(p[None, :, None, :], (batch, C, S, B))",
-        "np.broadcast_to(p.T.reshape(-1)[:C * B].reshape(C, B)[None, :, None, :], (batch, C, S, B))"),
+        "np.broadcast_to(p[None, :, None, :], (batch, C, S, W))",
+        "np.broadcast_to(p.T.reshape(-1)[:C * W].reshape(C, W)[None, :, None, :], (batch, C, S, W))"),
     "mask ignored in the backward": [
-        ("r = np.where(m_n != 0, g_u * np.sign(d[t]) / zeta_n, 0.0)", "r = g_u * np.sign(d[t]) / zeta_n"),
+        ("live = np.repeat((m_n != 0) & (nrm[t] > 0.0), k, axis=1)", "live = np.repeat(nrm[t] > 0.0, k, axis=1)"),
         ('kstar_n = _per_neuron(rec["kappa"] * rec["m"], batch, C, S)',
          'kstar_n = _per_neuron(rec["kappa"], batch, C, S)')],
+    "branch norm without the square root": ("nrm[t] = np.sqrt((d[t] * d[t]).reshape(N, B, k).sum(axis=2))",
+                                            "nrm[t] = (d[t] * d[t]).reshape(N, B, k).sum(axis=2)"),
+    "compartments grouped with stride B": ("nrm[t] = np.sqrt((d[t] * d[t]).reshape(N, B, k).sum(axis=2))",
+                                           "nrm[t] = np.sqrt((d[t] * d[t]).reshape(N, k, B).sum(axis=1))"),
+    "branch gradient spread with stride B": ("r = np.where(live, np.repeat(g_u, k, axis=1)",
+                                             "r = np.where(live, np.tile(g_u, (1, k))"),
+    "norm gradient divides by the squared norm": (
+        "unit = np.where(live, d[t] / np.where(live, np.repeat(nrm[t], k, axis=1), 1.0), 0.0)",
+        "unit = np.where(live, d[t] / np.where(live, np.repeat(nrm[t] ** 2, k, axis=1), 1.0), 0.0)"),
     "g_zeta missing 1/zeta": ("-g_u * u[t] / zeta_n", "-g_u * u[t]"),
     "sigmoid surrogate scale dropped": ("return scale * s * (1.0 - s)", "return s * (1.0 - s)"),
-    "residual gradient dropped": ('gX[t] = lam + dH[t][:, None] / B if rec["residual"] else lam',
+    "residual gradient dropped": ('gX[t] = lam + dH[t][:, None] / P if rec["residual"] else lam',
                                   'gX[t] = lam'),
-    "residual uses the sum, not the mean": ("Z[t] = Z[t] + X[t].mean(axis=1)", "Z[t] = Z[t] + X[t].sum(axis=1)"),
+    "residual uses the sum, not the mean": ("Z[t] = Z[t] + X[t].sum(axis=1) / P", "Z[t] = Z[t] + X[t].sum(axis=1)"),
+    "residual divides by the branch count": ("Z[t] = Z[t] + X[t].sum(axis=1) / P", "Z[t] = Z[t] + X[t].sum(axis=1) / B"),
     "g_beta uses H[t] instead of H[t-1]": ("t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]",
                                            "t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t]"),
     "g_beta ignores the reset": ("t_beta[t] = dH[t] * (1.0 - Sp[t - 1]) * H[t - 1]",
@@ -46,14 +56,18 @@ PIN_CALLS = [
     lambda: pins.test_worked_example_backward_vs_autograd("sigmoid", False),
     lambda: pins.test_single_step_closed_form("mexhat", "atan"),
     lambda: pins.test_constant_drive_mexican_hat_zero_input(),
-    lambda: pins.test_forward_matches_scalar_stepper("mexhat", True, True),
-    lambda: pins.test_forward_matches_scalar_stepper("identity", False, False),
-    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, False),
-    lambda: pins.test_backward_matches_autograd("identity", "atan", False, False, True, False),
+    lambda: pins.test_forward_matches_scalar_stepper("mexhat", True, True, 1),
+    lambda: pins.test_forward_matches_scalar_stepper("identity", False, False, 1),
+    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, False, 1),
+    lambda: pins.test_backward_matches_autograd("identity", "atan", False, False, True, False, 1),
     lambda: pins.test_mask_invariants(),
-    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, True),
+    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, True, 1),
     lambda: pins.test_residual_with_zero_strengths_is_lif_of_the_mean_input(),
     lambda: pins.test_plif_beta_gradient_of_a_free_leak(),
+    lambda: pins.test_two_compartment_worked_example_by_hand(),
+    lambda: pins.test_forward_matches_scalar_stepper("mexhat", True, True, 3),
+    lambda: pins.test_backward_matches_autograd("mexhat", "sigmoid", False, True, True, False, 2),
+    lambda: pins.test_backward_matches_autograd("identity", "atan", False, True, False, True, 3),
 ]
 
 

@@ -44,17 +44,19 @@ WORKED = dict(alpha=0.5, beta=0.5, v_th=1.0, kappa=np.array([[0.5, 0.25]]),
 
 
 def rand_case(rng, T=5, batch=2, C=3, S=2, B=3, psi_kind=PSI_MEXHAT, stateful=True,
-              mask=False, scale=1.0, residual=False):
+              mask=False, scale=1.0, residual=False, k=1):
+    """k compartments per branch: X is [T, N, B k], xi is [C, B k]."""
     N = batch * C * S
-    X = rng.normal(0.0, scale, size=(T, N, B))
+    X = rng.normal(0.0, scale, size=(T, N, B * k))
     kappa = rng.uniform(0.0, 1.0, size=(C, B)) + 0.3
-    xi = rng.normal(0.0, 0.5, size=(C, B))
+    xi = rng.normal(0.0, 0.5, size=(C, B * k))
     zeta = rng.uniform(0.5, 2.0, size=(C, B))
     m = (rng.random((C, B)) < 0.6).astype(np.uint8) if mask else None
     gS = rng.normal(size=(T, N))
     gV = rng.normal(size=(T, N))
     return dict(X=X, kappa=kappa, xi=xi, zeta=zeta, mask=m, gS=gS, gV=gV, C=C, S=S,
-                psi_kind=psi_kind, stateful=stateful, alpha=0.6, beta=0.7, v_th=1.0, residual=residual)
+                psi_kind=psi_kind, stateful=stateful, alpha=0.6, beta=0.7, v_th=1.0, residual=residual,
+                k=k)
 
 
 def run_oracle(case, force=None):
@@ -62,7 +64,8 @@ def run_oracle(case, force=None):
                           kappa=case["kappa"], xi=case["xi"], zeta=case["zeta"],
                           mask=case["mask"], C=case["C"], S=case["S"],
                           psi_kind=case["psi_kind"], stateful=case["stateful"],
-                          residual=case.get("residual", False), force=force)
+                          residual=case.get("residual", False), comps_per_branch=case.get("k", 1),
+                          force=force)
 
 
 # ---------------------------------------------------------------------------
@@ -304,21 +307,26 @@ def test_zero_input_identity_is_silent():
 # ---------------------------------------------------------------------------
 def scalar_stepper(case):
     X = case["X"]
-    T, N, B = X.shape
+    T, N, P = X.shape
+    k = case.get("k", 1)
+    B = P // k
     C, S = case["C"], case["S"]
     H = np.zeros((T, N))
     Sp = np.zeros((T, N))
     for n in range(N):
         c = (n // S) % C
-        vd = [0.0] * B
+        vd = [0.0] * P
         h = s = 0.0
         for t in range(T):
             z = 0.0
             for b in range(B):
-                vd[b] = case["alpha"] * vd[b] + X[t, n, b] if case["stateful"] else X[t, n, b]
-                xi = 0.0 if case["xi"] is None else case["xi"][c, b]
+                ss = 0.0
+                for i in range(b * k, (b + 1) * k):   # the compartments on branch b
+                    vd[i] = case["alpha"] * vd[i] + X[t, n, i] if case["stateful"] else X[t, n, i]
+                    xi = 0.0 if case["xi"] is None else case["xi"][c, i]
+                    ss += (vd[i] - xi) ** 2
                 ze = 1.0 if case["zeta"] is None else case["zeta"][c, b]
-                uu = abs(vd[b] - xi) / ze
+                uu = math.sqrt(ss) / ze
                 y = (1.0 - uu * uu) * math.exp(-0.5 * uu * uu) if case["psi_kind"] == PSI_MEXHAT else uu
                 on = case["mask"] is None or case["mask"][c, b] != 0
                 z += case["kappa"][c, b] * y if on else 0.0
@@ -331,10 +339,11 @@ def scalar_stepper(case):
 @pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
 @pytest.mark.parametrize("stateful", [True, False])
 @pytest.mark.parametrize("mask", [False, True])
-def test_forward_matches_scalar_stepper(psi_kind, stateful, mask):
+@pytest.mark.parametrize("k", [1, 3])
+def test_forward_matches_scalar_stepper(psi_kind, stateful, mask, k):
     rng = np.random.default_rng(7)
     case = rand_case(rng, T=6, batch=2, C=3, S=2, B=4, psi_kind=psi_kind, stateful=stateful,
-                     mask=mask)
+                     mask=mask, k=k)
     rec = run_oracle(case)
     H, Sp = scalar_stepper(case)
     assert np.allclose(rec["H"], H, rtol=1e-12, atol=1e-13)
@@ -349,11 +358,13 @@ def autograd_grads(case, sg_kind, sg_scale, detach_reset):
 
     torch_dtype = torch.float64
     X = torch.tensor(case["X"], dtype=torch_dtype, requires_grad=True)
-    T, N, B = X.shape
+    T, N, P = X.shape
+    k = case.get("k", 1)
+    B = P // k
     C, S = case["C"], case["S"]
     batch = N // (C * S)
     kappa = torch.tensor(case["kappa"], dtype=torch_dtype, requires_grad=True)
-    xi = torch.tensor(case["xi"] if case["xi"] is not None else np.zeros((C, B)),
+    xi = torch.tensor(case["xi"] if case["xi"] is not None else np.zeros((C, P)),
                       dtype=torch_dtype, requires_grad=True)
     zeta = torch.tensor(case["zeta"] if case["zeta"] is not None else np.ones((C, B)),
                         dtype=torch_dtype, requires_grad=True)
@@ -377,9 +388,10 @@ def autograd_grads(case, sg_kind, sg_scale, detach_reset):
             return g * sg_scale * sig * (1.0 - sig)
 
     def per_neuron(p):
-        return p[None, :, None, :].expand(batch, C, S, B).reshape(N, B)
+        w = p.shape[1]
+        return p[None, :, None, :].expand(batch, C, S, w).reshape(N, w)
 
-    vd = torch.zeros(N, B, dtype=torch_dtype)
+    vd = torch.zeros(N, P, dtype=torch_dtype)
     h = torch.zeros(N, dtype=torch_dtype)
     s = torch.zeros(N, dtype=torch_dtype)
     loss = torch.zeros((), dtype=torch_dtype)
@@ -387,7 +399,11 @@ def autograd_grads(case, sg_kind, sg_scale, detach_reset):
     gV = torch.tensor(case["gV"])
     for t in range(T):
         vd = alpha * vd + X[t] if case["stateful"] else X[t]
-        uu = torch.abs(vd - per_neuron(xi)) / per_neuron(zeta)
+        dv = vd - per_neuron(xi)
+        # branch b holds compartments b k .. b k + k - 1; torch's vector norm
+        # (subgradient 0 at the origin) for k > 1
+        nrm = torch.abs(dv) if k == 1 else torch.linalg.vector_norm(dv.reshape(N, B, k), dim=2)
+        uu = nrm / per_neuron(zeta)
         y = (1 - uu ** 2) * torch.exp(-uu ** 2 / 2) if case["psi_kind"] == PSI_MEXHAT else uu
         z = (per_neuron(kappa * m) * y).sum(dim=1)
         if case.get("residual", False):
@@ -419,13 +435,14 @@ def test_worked_example_backward_vs_autograd(sg_kind, detach_reset):
 @pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
 @pytest.mark.parametrize("sg_kind", [SG_ATAN, SG_SIGMOID])
 @pytest.mark.parametrize("detach_reset", [False, True])
-@pytest.mark.parametrize("stateful,mask,residual", [(True, False, False), (True, True, False),
-                                                   (False, True, False), (True, True, True),
-                                                   (False, False, True)])
-def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, mask, residual):
+@pytest.mark.parametrize("stateful,mask,residual,k", [(True, False, False, 1), (True, True, False, 1),
+                                                     (False, True, False, 1), (True, True, True, 1),
+                                                     (False, False, True, 1), (True, True, False, 2),
+                                                     (False, False, True, 4), (True, False, True, 3)])
+def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, mask, residual, k):
     rng = np.random.default_rng(8)
     case = rand_case(rng, T=6, batch=2, C=3, S=2, B=3, psi_kind=psi_kind, stateful=stateful,
-                     mask=mask, scale=1.2, residual=residual)
+                     mask=mask, scale=1.2, residual=residual, k=k)
     rec = run_oracle(case)
     g = oracle.backward(rec, case["gS"], case["gV"], sg_kind=sg_kind, sg_scale=3.0,
                         detach_reset=detach_reset)
@@ -436,8 +453,9 @@ def test_backward_matches_autograd(psi_kind, sg_kind, detach_reset, stateful, ma
     assert math.isclose(g["g_beta"], a["g_beta"], rel_tol=1e-11, abs_tol=1e-13)
     if mask:
         off = case["mask"] == 0
-        for k in ("g_kappa", "g_xi", "g_zeta"):
-            assert np.all(g[k][off] == 0.0)
+        for key in ("g_kappa", "g_zeta"):
+            assert np.all(g[key][off] == 0.0)
+        assert np.all(g["g_xi"][np.repeat(off, case["k"], axis=1)] == 0.0)
 
 
 # ---------------------------------------------------------------------------
@@ -458,7 +476,9 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
     zeta = case["zeta"] if zeta is None else zeta
     alpha = case["alpha"] if alpha is None else alpha
     beta = case["beta"] if beta is None else beta
-    T, N, B = X.shape
+    T, N, P = X.shape
+    k = case.get("k", 1)
+    B = P // k
     C, S = case["C"], case["S"]
     m = np.ones((C, B)) if case["mask"] is None else (case["mask"] != 0) * 1.0
     if sg_kind == SG_ATAN:
@@ -466,18 +486,20 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
     else:
         F = lambda v: special.expit(sg_scale * v)
     cidx = (np.arange(N) // S) % C
-    vd = np.zeros((N, B))
+    vd = np.zeros((N, P))
     h = np.zeros(N)
     s_t = np.zeros(N)
     s_b = np.zeros(N)
     loss = 0.0
     for t in range(T):
         vd = alpha * vd + X[t] if case["stateful"] else X[t]
-        uu = np.abs(vd - xi[cidx]) / zeta[cidx]
+        dv = vd - xi[cidx]
+        nrm = np.abs(dv) if k == 1 else np.sqrt(np.sum(dv.reshape(N, B, k) ** 2, axis=2))
+        uu = nrm / zeta[cidx]
         y = (1 - uu * uu) * np.exp(-0.5 * uu * uu) if case["psi_kind"] == PSI_MEXHAT else uu
         z = ((kappa * m)[cidx] * y).sum(axis=1)
         if case.get("residual", False):
-            z = z + X[t].sum(axis=1) / B
+            z = z + X[t].sum(axis=1) / P
         h = beta * (1 - (s_b if detach_reset else s_t)) * h + z
         s_t = base["S"][t] + F(h - case["v_th"]) - F(base["H"][t] - case["v_th"])
         s_b = base["S"][t]
@@ -488,11 +510,11 @@ def smooth_loss(case, base, sg_kind, sg_scale, detach_reset, X=None, kappa=None,
 @pytest.mark.parametrize("psi_kind", [PSI_MEXHAT, PSI_IDENTITY])
 @pytest.mark.parametrize("sg_kind", [SG_ATAN, SG_SIGMOID])
 @pytest.mark.parametrize("detach_reset", [False, True])
-@pytest.mark.parametrize("residual", [False, True])
-def test_backward_matches_finite_differences(psi_kind, sg_kind, detach_reset, residual):
+@pytest.mark.parametrize("residual,k", [(False, 1), (True, 1), (False, 2), (True, 3)])
+def test_backward_matches_finite_differences(psi_kind, sg_kind, detach_reset, residual, k):
     rng = np.random.default_rng(9)
     case = rand_case(rng, T=4, batch=1, C=2, S=2, B=3, psi_kind=psi_kind, mask=True, scale=1.2,
-                     residual=residual)
+                     residual=residual, k=k)
     rec = run_oracle(case)
     g = oracle.backward(rec, case["gS"], case["gV"], sg_kind=sg_kind, sg_scale=4.0,
                         detach_reset=detach_reset)
@@ -679,3 +701,87 @@ def test_plif_beta_gradient_of_a_free_leak():
     g = oracle.backward(rec, np.zeros((T, 1)), gV, sg_kind=SG_ATAN, detach_reset=True)
     assert math.isclose(rec["H"][-1, 0], beta ** (T - 1) * z, rel_tol=1e-14)
     assert math.isclose(g["g_beta"], (T - 1) * beta ** (T - 2) * z, rel_tol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# Several compartments per branch (Eq. methods-branch-aggregation, k = P/B > 1)
+# ---------------------------------------------------------------------------
+TWO_COMP = dict(alpha=0.5, beta=0.5, v_th=1.0, kappa=np.array([[0.5, 0.25]]),
+                xi=np.array([[0.0, 0.0, 2.0, 0.0]]), zeta=np.array([[10.0, 4.0]]), mask=None, C=1, S=1,
+                psi_kind=PSI_IDENTITY, comps_per_branch=2)
+TWO_COMP_X = np.array([[3.0, 4.0, 0.0, 0.0], [4.5, 6.0, 5.0, 4.0]])[:, None, :]
+
+
+def test_two_compartment_worked_example_by_hand():
+    """B = 2 branches of k = 2 compartments (compartments 0, 1 on branch 0 and 2, 3 on
+    branch 1), Identity, worked out by hand; every value is a dyadic rational.
+      t = 1: Vd = (3, 4, 0, 0), d = Vd - xi = (3, 4, -2, 0), norms (5, 2), u = (1/2, 1/2),
+             Z = 0.5/2 + 0.25/2 = 0.375 = H1, no spike.
+      t = 2: Vd = (6, 8, 5, 4), d = (6, 8, 3, 4), norms (10, 5), u = (1, 5/4),
+             Z = 0.5 + 0.3125, H2 = 0.375/2 + 0.8125 = 1: a tie, which fires.
+    Backward with gS = 1, gV = 0, atan surrogate, full reset gradient:
+      dH2 = sg(0) = 1;  dS1 = 1 - beta H1 dH2 = 0.8125;  dH1 = q dS1 + beta dH2,
+      q = sg(H1 - 1) = 1 / (1 + pi^2 (5/8)^2);
+      r_i = kappa_b dH d_i / (zeta_b ||d_b||),  lam = r + alpha lam[t+1]."""
+    rec = oracle.forward(TWO_COMP_X, **TWO_COMP)
+    assert np.array_equal(rec["H"][:, 0], [0.375, 1.0])
+    assert np.array_equal(rec["S"][:, 0], [0.0, 1.0])
+    assert np.array_equal(rec["u"][:, 0, :], [[0.5, 0.5], [1.0, 1.25]])
+    g = oracle.backward(rec, np.ones((2, 1)), sg_kind=SG_ATAN)
+    q = 1.0 / (1.0 + math.pi ** 2 * 0.390625)
+    dH2 = 1.0
+    dH1 = q * 0.8125 + 0.5 * dH2
+    assert np.allclose(g["dH"][:, 0], [dH1, dH2], rtol=1e-14, atol=0)
+    r2 = np.array([0.5 * 6 / 100, 0.5 * 8 / 100, 0.25 * 3 / 20, 0.25 * 4 / 20])
+    r1 = dH1 * np.array([0.5 * 3 / 50, 0.5 * 4 / 50, 0.25 * -2 / 8, 0.0])
+    lam2 = r2
+    lam1 = r1 + 0.5 * lam2
+    assert np.allclose(g["gX"][:, 0, :], [lam1, lam2], rtol=1e-14, atol=1e-300)
+    assert np.allclose(g["g_xi"][0], -(r1 + r2), rtol=1e-14)
+    assert np.allclose(g["g_kappa"][0], [dH1 * 0.5 + 1.0, dH1 * 0.5 + 1.25], rtol=1e-14)
+    assert np.allclose(g["g_zeta"][0], [-(0.5 * dH1 * 0.5 / 10 + 0.5 * 1.0 / 10),
+                                        -(0.25 * dH1 * 0.5 / 4 + 0.25 * 1.25 / 4)], rtol=1e-14)
+    assert math.isclose(g["g_alpha"], lam2 @ np.array([3.0, 4.0, 0.0, 0.0]), rel_tol=1e-14)
+    assert math.isclose(g["g_beta"], dH2 * 0.375, rel_tol=1e-14)
+
+
+def test_replicated_compartments_equal_one_with_scaled_dilation():
+    """k identical compartments (same input, same xi) have norm sqrt(k) |d|, so the layer
+    equals the one-compartment layer with zeta / sqrt(k); the input gradient splits evenly
+    over the k copies, xi's likewise, and zeta's scales by 1/sqrt(k)."""
+    rng = np.random.default_rng(30)
+    k = 4
+    base = rand_case(rng, T=6, B=3, mask=True, psi_kind=PSI_MEXHAT, k=1)
+    rep_case = dict(base, X=np.repeat(base["X"], k, axis=2), xi=np.repeat(base["xi"], k, axis=1), k=k)
+    one = dict(base, zeta=base["zeta"] / math.sqrt(k))
+    a, b = run_oracle(rep_case), run_oracle(one)
+    assert np.allclose(a["H"], b["H"], rtol=1e-12, atol=1e-13)
+    assert np.array_equal(a["S"], b["S"])
+    ga = oracle.backward(a, base["gS"], base["gV"], sg_kind=SG_SIGMOID)
+    gb = oracle.backward(b, base["gS"], base["gV"], sg_kind=SG_SIGMOID)
+    T, N = base["gS"].shape
+    assert np.allclose(ga["gX"].reshape(T, N, 3, k), gb["gX"][..., None] / k, rtol=1e-10, atol=1e-13)
+    assert np.allclose(ga["g_xi"].reshape(base["C"], 3, k), gb["g_xi"][..., None] / k, rtol=1e-10, atol=1e-13)
+    assert np.allclose(ga["g_zeta"], gb["g_zeta"] / math.sqrt(k), rtol=1e-10, atol=1e-13)
+    assert np.allclose(ga["g_kappa"], gb["g_kappa"], rtol=1e-10, atol=1e-13)
+    assert math.isclose(ga["g_alpha"], gb["g_alpha"], rel_tol=1e-10)
+
+
+def test_compartment_order_within_a_branch_does_not_matter():
+    """The norm is symmetric in a branch's compartments: permuting them (with their xi)
+    permutes gX and g_xi and leaves everything else alone; moving a compartment to
+    another branch changes the result."""
+    rng = np.random.default_rng(31)
+    k, B = 3, 2
+    case = rand_case(rng, T=5, B=B, k=k, mask=False)
+    perm = np.concatenate([b * k + rng.permutation(k) for b in range(B)])
+    c2 = dict(case, X=case["X"][:, :, perm], xi=case["xi"][:, perm])
+    a, b = run_oracle(case), run_oracle(c2)
+    assert np.allclose(a["H"], b["H"], rtol=1e-13) and np.array_equal(a["S"], b["S"])
+    ga, gb = oracle.backward(a, case["gS"], case["gV"]), oracle.backward(b, case["gS"], case["gV"])
+    assert np.allclose(gb["gX"], ga["gX"][:, :, perm], rtol=1e-12, atol=1e-14)
+    assert np.allclose(gb["g_xi"], ga["g_xi"][:, perm], rtol=1e-12, atol=1e-14)
+    swap = np.arange(B * k)
+    swap[[0, k]] = swap[[k, 0]]   # compartment 0 to branch 1 and back
+    c3 = dict(case, X=case["X"][:, :, swap], xi=case["xi"][:, swap])
+    assert not np.allclose(run_oracle(c3)["H"], a["H"], rtol=1e-6)
