@@ -7,8 +7,9 @@
  * and Robust Deep Spiking Neural Networks" (Huang et al., arXiv 2412.06355):
  *
  *   Methods, "Dendritic spiking neuron":
- *     Eq. (methods-compartment)        Vd_b[t] = alpha Vd_b[t-1] + X_b[t],  Vd[0] = 0
- *     Eq. (methods-branch-aggregation) Y_b[t]  = psi(|Vd_b[t] - xi_b| / zeta_b)   (one compartment per branch)
+ *     Eq. (methods-compartment)        Vd_i[t] = alpha Vd_i[t-1] + X_i[t],  Vd[0] = 0
+ *     Eq. (methods-branch-aggregation) Y_b[t]  = psi(||Vd_{C_b}[t] - xi_{C_b}|| / zeta_b), the L2 norm
+ *                                      over the KC = comps_per_branch compartments of branch b
  *     Eq. (methods-mexican-hat)        psi(x)  = (1 - x^2) exp(-x^2/2), or psi(x) = x
  *     Eq. (methods-soma-input)         Z[t]    = sum_b kappa_b Y_b[t]
  *     Eq. (methods-lif-reset-charge)   H[t]    = beta (1 - S[t-1]) H[t-1] + Z[t],  H[0] = S[0] = 0
@@ -24,11 +25,13 @@
  *     channel share xi, zeta, kappa; alpha is shared by the whole layer; the
  *     backward replaces Theta' by a surrogate derivative, Eq. (methods-sg).
  *
- * Layout (all row-major):
- *   X, grad_x          [T, N, B]  branches innermost, I/O dtype (fp32 or bf16)
+ * Layout (all row-major), with P = B * KC compartments per neuron:
+ *   X, grad_x          [T, N, P]  compartments innermost, I/O dtype (fp32 or bf16); compartment
+ *                                 i lies on branch i / KC (a branch's compartments are adjacent)
  *   spikes, grad_spikes[T, N]     I/O dtype; spikes are exactly 0.0 or 1.0
  *   v_soma, grad_v_soma[T, N]     fp32; v_soma[t] = H[t], the potential before the reset
- *   kappa, xi, zeta    [C, B]     fp32 per-channel parameters
+ *   kappa, zeta        [C, B]     fp32 per-channel branch parameters
+ *   xi                 [C, P]     fp32 per-channel compartment translations
  *   mask               [C, B]     uint8, nonzero = branch kept
  *   alpha              [1]        fp32 on the device (a learnable layer scalar)
  *   beta               [1]        fp32 on the device, optional: a learnable somatic decay
@@ -82,7 +85,7 @@ typedef struct dendsn_cfg {
     int64_t C;                 /* channels (parameter sets), >= 1                          */
     int64_t S;                 /* spatial positions per channel, >= 1 (1 = fully connected)*/
     int32_t B;                 /* branches per neuron, 1..128                              */
-    int32_t comps_per_branch;  /* compartments per branch (P / B); must be 1               */
+    int32_t comps_per_branch;  /* compartments per branch KC = P / B: 1, 2 or 4            */
     int32_t stateful;          /* 1: leaky compartments; 0: Stateless Dendrite             */
     int32_t detach_reset;      /* 1: no gradient through the reset factor (1 - S[t-1])     */
     int32_t ckpt_every;        /* K >= 1: state checkpoint after every K steps (K >= T: none) */
@@ -98,7 +101,7 @@ typedef struct dendsn_cfg {
 
 /*
  * Size in bytes of the state-checkpoint buffer that dendsn_forward fills and
- * dendsn_backward reads: nck * N * (B + 1) * 4 with nck = ceil(T / K) - 1
+ * dendsn_backward reads: nck * N * (P + 1) * 4 with nck = ceil(T / K) - 1
  * (the dendritic state and the somatic potential after steps K, 2K, ... < T).
  * Zero when K >= T.  Returns DENDSN_E_INVALID / _UNSUPPORTED for a bad cfg.
  */
@@ -113,12 +116,12 @@ dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes);
 
 /*
  * Forward scan over t = 1..T (equations above).
- *   x       [T,N,B] io    required
+ *   x       [T,N,P] io    required
  *   alpha   [1] fp32      required when cfg->stateful, ignored otherwise
  *   beta    [1] fp32      optional learnable somatic decay (NULL: cfg->beta)
  *   kappa   [C,B] fp32    required (for dendritic branch gating with per-task dense
  *                         strengths, DBG_e, pass the task's own [C,B] table)
- *   xi      [C,B] fp32    NULL means 0
+ *   xi      [C,P] fp32    NULL means 0
  *   zeta    [C,B] fp32    NULL means 1
  *   mask    [C,B] uint8   NULL means every branch kept
  *   spikes  [T,N] io      required output
@@ -140,13 +143,13 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
  *   ckpt         required when nck > 0 (see dendsn_ckpt_bytes)
  *   grad_spikes  [T,N] io     required
  *   grad_v_soma  [T,N] fp32   NULL means 0
- *   grad_x       [T,N,B] io   required output (with the residual dendrite it includes the
+ *   grad_x       [T,N,P] io   required output (with the residual dendrite it includes the
  *                dH/P of the residual path, also on gated-off branches)
  *   grad_alpha   [1] fp32     optional output (0 for the Stateless Dendrite)
  *   grad_beta    [1] fp32     optional output: d/d beta of the loss (PLIF soma), summed
  *                over time and neurons; meaningful whether beta came from cfg or the device
- *   grad_kappa, grad_xi, grad_zeta  [C,B] fp32 optional outputs, summed over
- *                time, batch and spatial positions; exactly 0 where the mask is 0.
+ *   grad_kappa, grad_zeta [C,B], grad_xi [C,P]  fp32 optional outputs, summed over
+ *                time, batch and spatial positions; exactly 0 for gated-off branches.
  *   workspace    device scratch of at least dendsn_bwd_workspace_bytes bytes,
  *                clobbered by the call.
  * Results are deterministic: the same inputs give bit-identical outputs.

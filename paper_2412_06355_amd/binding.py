@@ -55,7 +55,8 @@ class dendsn_cfg(ctypes.Structure):
 
 @dataclass(frozen=True)
 class DendSNConfig:
-    """One DendSN layer: N = batch * C * S neurons with B branches, T steps."""
+    """One DendSN layer: N = batch * C * S neurons with B branches of
+    comps_per_branch compartments each (P in all), T steps."""
 
     T: int
     batch: int
@@ -78,6 +79,11 @@ class DendSNConfig:
     @property
     def N(self) -> int:
         return self.batch * self.C * self.S
+
+    @property
+    def P(self) -> int:
+        """Compartments per neuron: the innermost extent of X and grad_x."""
+        return self.B * self.comps_per_branch
 
     def with_(self, **kw) -> "DendSNConfig":
         return dataclasses.replace(self, **kw)
@@ -211,11 +217,11 @@ def _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta=None):
     import torch
 
     dev = x.device
-    _expect(x, "x", (cfg.T, cfg.N, cfg.B), _io_dtype(cfg), dev)
+    _expect(x, "x", (cfg.T, cfg.N, cfg.P), _io_dtype(cfg), dev)
     _expect(alpha, "alpha", (1,), torch.float32, dev, optional=not cfg.stateful)
     _expect(beta, "beta", (1,), torch.float32, dev, optional=True)
     _expect(kappa, "kappa", (cfg.C, cfg.B), torch.float32, dev)
-    _expect(xi, "xi", (cfg.C, cfg.B), torch.float32, dev, optional=True)
+    _expect(xi, "xi", (cfg.C, cfg.P), torch.float32, dev, optional=True)
     _expect(zeta, "zeta", (cfg.C, cfg.B), torch.float32, dev, optional=True)
     _expect(mask, "mask", (cfg.C, cfg.B), torch.uint8, dev, optional=True)
 
@@ -238,8 +244,8 @@ def forward(cfg: DendSNConfig, x, alpha, kappa, xi=None, zeta=None, mask=None, *
 
 def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma=None,
              workspace=None, *, beta=None):
-    """Returns a dict with grad_x [T,N,B] io and grad_alpha [1], grad_beta [1],
-    grad_kappa, grad_xi, grad_zeta [C,B] (fp32)."""
+    """Returns a dict with grad_x [T,N,P] io and grad_alpha [1], grad_beta [1],
+    grad_kappa, grad_zeta [C,B] and grad_xi [C,P] (fp32)."""
     import torch
 
     _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta)
@@ -247,11 +253,11 @@ def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spik
     _expect(grad_spikes, "grad_spikes", (cfg.T, cfg.N), _io_dtype(cfg), dev)
     _expect(grad_v_soma, "grad_v_soma", (cfg.T, cfg.N), torch.float32, dev, optional=True)
     out = dict(
-        grad_x=torch.empty((cfg.T, cfg.N, cfg.B), dtype=_io_dtype(cfg), device=dev),
+        grad_x=torch.empty((cfg.T, cfg.N, cfg.P), dtype=_io_dtype(cfg), device=dev),
         grad_alpha=torch.empty((1,), dtype=torch.float32, device=dev),
         grad_beta=torch.empty((1,), dtype=torch.float32, device=dev),
         grad_kappa=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
-        grad_xi=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
+        grad_xi=torch.empty((cfg.C, cfg.P), dtype=torch.float32, device=dev),
         grad_zeta=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),
     )
     if workspace is None:

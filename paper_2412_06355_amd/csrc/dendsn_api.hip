@@ -14,13 +14,19 @@ hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int psi, hipStream_
 hipError_t launch_fwd_bf16(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream);
 hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
 hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_fwd_f32_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
+hipError_t launch_fwd_bf16_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
 
 // Fixed-order float64 sums of the per-block partials into the parameter
-// gradients.  Outputs o = (c * 3 + q) * B + b, q = 0, 1, 2 for kappa, xi, zeta.
-// The last block reduces the g_alpha partials.
+// gradients.  Outputs o = c * W + ol with W = 2 B + P: ol < B is g_kappa of
+// branch ol, then g_xi of the P compartments, then g_zeta of the B branches.
+// The last block reduces the g_alpha partials, the one before g_beta's.
 __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   const int tid = threadIdx.x;
-  const int64_t nout = f.C * 3 * f.B;
+  const int W = 2 * f.B + f.P;
+  const int64_t nout = f.C * W;
   if (blockIdx.x >= gridDim.x - 2) {  // last block: g_alpha; the one before: g_beta
     const bool is_alpha = blockIdx.x == gridDim.x - 1;
     const float* src = is_alpha ? f.wsA : f.wsB;
@@ -45,21 +51,29 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
     o = int64_t(blockIdx.x) * (kThreads / 64) + (tid >> 6);
     const int lane = tid & 63;
     if (o < nout)
-      for (int64_t p = lane; p < f.P; p += 64) s += double(f.wsP[o * f.P + p]);
+      for (int64_t p = lane; p < f.slots; p += 64) s += double(f.wsP[o * f.slots + p]);
     for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
     if (lane != 0 || o >= nout) return;
   } else {       // one thread per output, slots in order
     o = int64_t(blockIdx.x) * kThreads + tid;
     if (o >= nout) return;
-    for (int64_t p = 0; p < f.P; ++p) s += double(f.wsP[p * nout + o]);
+    for (int64_t p = 0; p < f.slots; ++p) s += double(f.wsP[p * nout + o]);
   }
-  const int64_t c = o / (3 * f.B);
-  const int q = int((o / f.B) % 3);
-  const int b = int(o % f.B);
-  float* out = q == 0 ? f.gk : (q == 1 ? f.gxi : f.gz);
+  const int64_t c = o / W;
+  const int ol = int(o % W);
+  float* out;
+  int64_t idx;
+  int b;  // the branch the output belongs to
+  if (ol < f.B) {
+    out = f.gk; idx = c * f.B + ol; b = ol;
+  } else if (ol < f.B + f.P) {
+    out = f.gxi; idx = c * f.P + (ol - f.B); b = (ol - f.B) / f.KC;
+  } else {
+    out = f.gz; idx = c * f.B + (ol - f.B - f.P); b = ol - f.B - f.P;
+  }
   if (!out) return;
   const bool on = f.mask ? (f.mask[c * f.B + b] != 0) : true;
-  out[c * f.B + b] = on ? float(s) : 0.0f;
+  out[idx] = on ? float(s) : 0.0f;
 }
 
 }  // namespace dendsn
@@ -79,19 +93,35 @@ bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// (BL, L): a vector-width lane split when the branch count allows one, else a
-// generic split with up to 8 branches per lane over 1 or 2 lanes.
-bool choose_mapping(int B, int io, int* BL, int* L, int* fast) {
-  const int blv = (io == DENDSN_IO_BF16 && B % 8 == 0) ? 8 : 4;
+// (BL, L) for KC compartments per branch.  KC = 1: a vector-width lane split
+// when the branch count allows one, else a generic split with up to 8 branches
+// per lane over 1 or 2 lanes.  KC = 2 or 4: 16 bytes of compartments per lane
+// (BL KC = 4 for fp32, 8 for bf16) when the branch count allows, else one lane
+// holds the whole neuron (B KC <= 14).
+bool choose_mapping(int B, int KC, int io, int* BL, int* L, int* fast) {
+  if (KC == 1) {
+    const int blv = (io == DENDSN_IO_BF16 && B % 8 == 0) ? 8 : 4;
+    if (B % blv == 0 && is_pow2(B / blv) && B / blv <= 16) {
+      *BL = blv; *L = B / blv; *fast = 1;
+      return true;
+    }
+    for (int l = 1; l <= 2; l *= 2) {
+      if (B % l == 0 && B / l <= 8) {
+        *BL = B / l; *L = l; *fast = 0;
+        return true;
+      }
+    }
+    return false;
+  }
+  if (KC != 2 && KC != 4) return false;
+  const int blv = (io == DENDSN_IO_BF16 ? 8 : 4) / KC;
   if (B % blv == 0 && is_pow2(B / blv) && B / blv <= 16) {
     *BL = blv; *L = B / blv; *fast = 1;
     return true;
   }
-  for (int l = 1; l <= 2; l *= 2) {
-    if (B % l == 0 && B / l <= 8) {
-      *BL = B / l; *L = l; *fast = 0;
-      return true;
-    }
+  if ((KC == 2 && B <= 7 && B != 4) || (KC == 4 && B <= 3)) {
+    *BL = B; *L = 1; *fast = 0;
+    return true;
   }
   return false;
 }
@@ -106,8 +136,8 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   if (c->S < 1) return fail(DENDSN_E_INVALID, "S must be >= 1");
   if (c->B < 1 || c->B > 128) return fail(DENDSN_E_INVALID, "B must be in [1, 128]");
   if (c->comps_per_branch < 1) return fail(DENDSN_E_INVALID, "comps_per_branch must be >= 1");
-  if (c->comps_per_branch != 1)
-    return fail(DENDSN_E_UNSUPPORTED, "only one compartment per branch (P == B) is supported");
+  if (c->comps_per_branch != 1 && c->comps_per_branch != 2 && c->comps_per_branch != 4)
+    return fail(DENDSN_E_UNSUPPORTED, "comps_per_branch must be 1, 2 or 4");
   if (c->stateful != 0 && c->stateful != 1) return fail(DENDSN_E_INVALID, "stateful must be 0 or 1");
   if (c->detach_reset != 0 && c->detach_reset != 1)
     return fail(DENDSN_E_INVALID, "detach_reset must be 0 or 1");
@@ -125,9 +155,10 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   const int64_t lim = int64_t(1) << 46;
   if (c->batch > lim / c->C || c->batch * c->C > lim / c->S) return fail(DENDSN_E_INVALID, "N too large");
   const int64_t N = c->batch * c->C * c->S;
-  if (N > (lim / c->B) / c->T) return fail(DENDSN_E_INVALID, "T * N * B too large");
+  const int64_t P = int64_t(c->B) * c->comps_per_branch;
+  if (N > (lim / P) / c->T) return fail(DENDSN_E_INVALID, "T * N * P too large");
   int BL, L, fast;
-  if (!choose_mapping(c->B, c->io, &BL, &L, &fast))
+  if (!choose_mapping(c->B, c->comps_per_branch, c->io, &BL, &L, &fast))
     return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build");
   return DENDSN_OK;
 }
@@ -137,7 +168,8 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
 Plan make_plan(const dendsn_cfg* c, bool bwd) {
   Plan p;
   memset(&p, 0, sizeof(p));
-  choose_mapping(c->B, c->io, &p.BL, &p.L, &p.fast);
+  choose_mapping(c->B, c->comps_per_branch, c->io, &p.BL, &p.L, &p.fast);
+  p.KC = c->comps_per_branch;
   const int L = p.L;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
@@ -167,17 +199,17 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   p.G = int32_t(ceil_div(c->batch, p.bpg));
   const int64_t Ke = c->ckpt_every < c->T ? c->ckpt_every : c->T;
   p.nck = int32_t(ceil_div(c->T, c->ckpt_every) - 1);
-  p.KS = (p.fast && p.BL <= 4 && Ke >= 8) ? 8 : 4;
+  p.KS = (p.fast && p.KC == 1 && p.BL <= 4 && Ke >= 8) ? 8 : 4;
   return p;
 }
 
 size_t ckpt_bytes(const dendsn_cfg* c, const Plan& p) {
   const int64_t N = c->batch * c->C * c->S;
-  return size_t(p.nck) * size_t(N) * size_t(c->B + 1) * sizeof(float);
+  return size_t(p.nck) * size_t(N) * size_t(c->B * c->comps_per_branch + 1) * sizeof(float);
 }
 
 void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) {
-  const size_t nP = size_t(p.G) * size_t(p.tpc) * size_t(c->C) * 3 * size_t(c->B);
+  const size_t nP = size_t(p.G) * size_t(p.tpc) * size_t(c->C) * size_t(2 * c->B + c->B * c->comps_per_branch);
   const size_t nA = size_t(p.G) * size_t(p.ntiles);
   *offA = ((nP * sizeof(float) + 255) / 256) * 256;
   *total = *offA + 2 * nA * sizeof(float);  // g_alpha partials, then g_beta partials
@@ -185,10 +217,11 @@ void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) 
 
 dendsn_status check_grid(const dendsn_cfg* c, const Plan& p) {
   if (p.ntiles * p.G > int64_t(INT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "grid too large");
-  if (c->C * 3 * c->B / (kThreads / 64) + 2 > int64_t(INT32_MAX))
+  const int64_t P = int64_t(c->B) * c->comps_per_branch;
+  if (c->C * (2 * c->B + P) / (kThreads / 64) + 2 > int64_t(INT32_MAX))
     return fail(DENDSN_E_UNSUPPORTED, "too many parameter-gradient outputs");
   // per-lane byte offsets inside one sample's slice are 32-bit
-  if (c->C * c->S * c->B * 4 > int64_t(UINT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "sample slice above 4 GiB");
+  if (c->C * c->S * P * 4 > int64_t(UINT32_MAX)) return fail(DENDSN_E_UNSUPPORTED, "sample slice above 4 GiB");
   return DENDSN_OK;
 }
 
@@ -202,6 +235,7 @@ void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* a
   s->T = c->T; s->C = c->C; s->S = c->S; s->batch = c->batch;
   s->M = c->C * c->S; s->N = c->batch * s->M;
   s->B = c->B;
+  s->P = c->B * c->comps_per_branch;
   s->K = int32_t(c->ckpt_every < c->T ? c->ckpt_every : c->T);
   s->nck = p.nck;
   s->beta = c->beta; s->vth = c->v_th;
@@ -272,8 +306,9 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   fa.vsoma = v_soma;
   fa.ckpt = p.nck > 0 ? ckpt : nullptr;
   const int v = cfg->psi | (cfg->residual << 1);
-  const hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_fwd_bf16(p, fa, v, stream)
-                                                 : launch_fwd_f32(p, fa, v, stream);
+  const bool bf = cfg->io == DENDSN_IO_BF16;
+  const hipError_t e = p.KC == 1 ? (bf ? launch_fwd_bf16(p, fa, v, stream) : launch_fwd_f32(p, fa, v, stream))
+                                 : (bf ? launch_fwd_bf16_kc(p, fa, v, stream) : launch_fwd_f32_kc(p, fa, v, stream));
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("forward launch: ") + hipGetErrorString(e));
   return DENDSN_OK;
 }
@@ -322,23 +357,25 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   ba.wsP = static_cast<float*>(workspace);
   ba.wsA = reinterpret_cast<float*>(static_cast<char*>(workspace) + offA);
   ba.wsB = ba.wsA + int64_t(p.G) * p.ntiles;
-  ba.P = int64_t(p.G) * p.tpc;
-  ba.wide = ba.P > kNarrowSlots;
+  ba.slots = int64_t(p.G) * p.tpc;
+  ba.wide = ba.slots > kNarrowSlots;
   ba.detach = cfg->detach_reset;
   ba.sg = cfg->sg;
   ba.sg_scale = cfg->sg_scale;
   const int v = cfg->psi | (cfg->residual << 1);
-  hipError_t e = cfg->io == DENDSN_IO_BF16 ? launch_bwd_bf16(p, ba, v, stream)
-                                           : launch_bwd_f32(p, ba, v, stream);
+  const bool bf = cfg->io == DENDSN_IO_BF16;
+  hipError_t e = p.KC == 1 ? (bf ? launch_bwd_bf16(p, ba, v, stream) : launch_bwd_f32(p, ba, v, stream))
+                           : (bf ? launch_bwd_bf16_kc(p, ba, v, stream) : launch_bwd_f32_kc(p, ba, v, stream));
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("backward launch: ") + hipGetErrorString(e));
 
   FinArgs f;
   memset(&f, 0, sizeof(f));
   f.wsP = ba.wsP; f.wsA = ba.wsA; f.wsB = ba.wsB; f.mask = mask;
   f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha; f.gb = grad_beta;
-  f.C = cfg->C; f.B = cfg->B; f.P = ba.P; f.wide = ba.wide; f.stateful = cfg->stateful;
+  f.C = cfg->C; f.B = cfg->B; f.P = ba.s.P; f.KC = p.KC; f.slots = ba.slots; f.wide = ba.wide;
+  f.stateful = cfg->stateful;
   f.nA = int64_t(p.G) * p.ntiles;
-  const int64_t nout = cfg->C * 3 * cfg->B;
+  const int64_t nout = cfg->C * (2 * cfg->B + ba.s.P);
   const int64_t nblk = (f.wide ? ceil_div(nout, kThreads / 64) : ceil_div(nout, kThreads)) + 2;
   dendsn_finalize_kernel<<<dim3(unsigned(nblk)), dim3(kThreads), 0, stream>>>(f);
   e = hipGetLastError();

@@ -26,9 +26,12 @@ namespace dendsn {
 typedef uint16_t bf16_t;  // bf16 storage
 
 // Kernel variant V: bit 0 = Mexican-hat activation (else identity), bit 1 =
-// residual dendrite (Z also receives the mean synaptic input of the neuron).
+// residual dendrite (Z also receives the mean synaptic input of the neuron),
+// bits 2-3 = log2 of the compartments per branch KC (1, 2 or 4).  A lane holds
+// BL branches, i.e. E = BL * KC consecutive compartments of its neuron.
 template <int V> constexpr bool kMH = (V & 1) != 0;
 template <int V> constexpr bool kRes = (V & 2) != 0;
+template <int V> constexpr int kKC = 1 << ((V >> 2) & 3);
 
 // -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.721347520444481703680f;
@@ -257,46 +260,69 @@ __device__ __forceinline__ float lane_sum(const float (&p)[BL]) {
 // ---------------------------------------------------------------------------
 // Per-lane branch parameters of one channel.
 // ---------------------------------------------------------------------------
-template <int BL>
+template <int BL, int KC>
 struct Branches {
-  float k[BL];   // kappa * m  (0 for a gated-off branch)
-  float xi[BL];
-  float rz[BL];  // 1 / zeta
-  bool on[BL];   // mask bit
-  float rp;      // 1 / P, the residual term's weight of each compartment
+  float k[BL];        // kappa * m  (0 for a gated-off branch)
+  float xi[BL * KC];  // per compartment
+  float rz[BL];       // 1 / zeta
+  bool on[BL];        // mask bit
+  float rp;           // 1 / P, the residual term's weight of each compartment
 };
 
-template <int BL>
-__device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int sub, Branches<BL>& br) {
+template <int BL, int KC>
+__device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int sub, Branches<BL, KC>& br) {
   const int64_t base = c * a.B + int64_t(sub) * BL;
 #pragma unroll
   for (int j = 0; j < BL; ++j) {
     const bool on = a.mask ? (a.mask[base + j] != 0) : true;
     br.on[j] = on;
     br.k[j] = on ? a.kappa[base + j] : 0.0f;
-    br.xi[j] = a.xi ? a.xi[base + j] : 0.0f;
     br.rz[j] = a.zeta ? 1.0f / a.zeta[base + j] : 1.0f;
   }
+  const int64_t base_i = c * a.P + int64_t(sub) * (BL * KC);
+#pragma unroll
+  for (int i = 0; i < BL * KC; ++i) br.xi[i] = a.xi ? a.xi[base_i + i] : 0.0f;
   br.rp = a.rP;
 }
 
+// Sum of squares of a branch's KC compartment offsets d = Vd - xi, in a fixed order.
+template <int KC>
+__device__ __forceinline__ float branch_sumsq(const float* vd, const float* xi) {
+  float d = vd[0] - xi[0];
+  float ss = d * d;
+#pragma unroll
+  for (int i = 1; i < KC; ++i) {
+    d = vd[i] - xi[i];
+    ss = fmaf(d, d, ss);
+  }
+  return ss;
+}
+
 // ---------------------------------------------------------------------------
-// One forward step of the dendrite (leaky compartments, L2 aggregation with one
-// compartment per branch, activation, weighted branch sum) and of the LIF soma.
-// A gated-off branch keeps a zero state, so nothing it receives can reach the
-// soma or its gradients.
+// One forward step of the dendrite (leaky compartments, L2 aggregation over
+// each branch's compartments, activation, weighted branch sum) and of the LIF
+// soma.  A gated-off branch keeps a zero state, so nothing it receives can
+// reach the soma or its gradients.
 // ---------------------------------------------------------------------------
 template <int BL, int L, int V>
-__device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv)[BL],
-                                               const Branches<BL>& br, float alpha,
+__device__ __forceinline__ float dendrite_step(float (&vd)[BL * kKC<V>], const float (&xv)[BL * kKC<V>],
+                                               const Branches<BL, kKC<V>>& br, float alpha,
                                                float* efac = nullptr) {
+  constexpr int KC = kKC<V>;
   float part[BL];
 #pragma unroll
   for (int j = 0; j < BL; ++j) {
-    float v = fmaf(alpha, vd[j], xv[j]);   // alpha = 0: Stateless Dendrite
-    v = br.on[j] ? v : 0.0f;
-    vd[j] = v;
-    const float tt = (v - br.xi[j]) * br.rz[j];   // signed (Vd - xi)/zeta; u = |tt|
+#pragma unroll
+    for (int i = j * KC; i < (j + 1) * KC; ++i) {
+      float v = fmaf(alpha, vd[i], xv[i]);   // alpha = 0: Stateless Dendrite
+      vd[i] = br.on[j] ? v : 0.0f;
+    }
+    // KC = 1: the signed (Vd - xi)/zeta, u = |tt|; else u = ||Vd - xi|| / zeta >= 0
+    float tt;
+    if constexpr (KC == 1)
+      tt = (vd[j] - br.xi[j]) * br.rz[j];
+    else
+      tt = __builtin_amdgcn_sqrtf(branch_sumsq<KC>(&vd[j * KC], &br.xi[j * KC])) * br.rz[j];
     float y;
     if constexpr (kMH<V>) {
       const float q = tt * tt;
@@ -304,12 +330,14 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL], const float (&xv
       if (efac) efac[j] = e;
       y = (1.0f - q) * e;
     } else {
-      y = fabsf(tt);
+      y = KC == 1 ? fabsf(tt) : tt;
     }
-    if constexpr (kRes<V>)
-      part[j] = fmaf(xv[j], br.rp, br.k[j] * y);  // every compartment feeds the residual
-    else
-      part[j] = br.k[j] * y;
+    float pj = br.k[j] * y;
+    if constexpr (kRes<V>) {
+#pragma unroll
+      for (int i = j * KC; i < (j + 1) * KC; ++i) pj = fmaf(xv[i], br.rp, pj);  // every compartment feeds the residual
+    }
+    part[j] = pj;
   }
   return group_sum<L>(lane_sum<BL>(part));
 }
@@ -378,11 +406,11 @@ struct LaneOff {
   uint32_t v;   // fp32 per-neuron rows (v_soma, grad_v_soma, checkpointed H)
 };
 
-template <typename IO, int BL>
+template <typename IO, int E>
 __device__ __forceinline__ LaneOff lane_offsets(const ScanArgs& a, const Pos& pos) {
   LaneOff o;
-  o.x = uint32_t((pos.m * a.B + pos.sub * BL) * int64_t(sizeof(IO)));
-  o.c = uint32_t((pos.m * a.B + pos.sub * BL) * 4);
+  o.x = uint32_t((pos.m * a.P + pos.sub * E) * int64_t(sizeof(IO)));
+  o.c = uint32_t((pos.m * a.P + pos.sub * E) * 4);
   o.s = uint32_t(pos.m * int64_t(sizeof(IO)));
   o.v = uint32_t(pos.m * 4);
   return o;
@@ -428,9 +456,9 @@ __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, 
 
 // Running state of the neuron a lane is computing, and wave-uniform output
 // pointers of its batch item (advanced step by step, never recomputed).
-template <typename IO, int BL>
+template <typename IO, int E>
 struct FwdLane {
-  float vd[BL];
+  float vd[E];
   float h;
   bool s;
   int t;          // step index of the chunk being computed (0 .. Tp-1)
@@ -441,25 +469,26 @@ struct FwdLane {
   float* ckh;     // next checkpoint's H row of this item
 };
 
-template <typename IO, int BL>
-__device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, FwdLane<IO, BL>& st) {
+template <typename IO, int E>
+__device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, FwdLane<IO, E>& st) {
   const ScanArgs& a = fa.s;
   st.t = 0;
   st.kc = a.K;
   st.sp = static_cast<IO*>(fa.spikes) + n0;
   st.vp = fa.vsoma ? fa.vsoma + n0 : nullptr;
-  st.ckv = fa.ckpt ? fa.ckpt + n0 * a.B : nullptr;
-  st.ckh = fa.ckpt ? fa.ckpt + int64_t(a.nck) * a.N * a.B + n0 : nullptr;
+  st.ckv = fa.ckpt ? fa.ckpt + n0 * a.P : nullptr;
+  st.ckh = fa.ckpt ? fa.ckpt + int64_t(a.nck) * a.N * a.P + n0 : nullptr;
 #pragma unroll
-  for (int j = 0; j < BL; ++j) st.vd[j] = 0.0f;
+  for (int j = 0; j < E; ++j) st.vd[j] = 0.0f;
   st.h = 0.0f;
   st.s = false;
 }
 
 template <typename IO, int BL, int L, int V, int D>
-__device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL>& br,
+__device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, bool lead, int T, int Tp, int64_t item_neurons,
-                                              const float (&buf)[D][BL], FwdLane<IO, BL>& st) {
+                                              const float (&buf)[D][BL * kKC<V>], FwdLane<IO, BL * kKC<V>>& st) {
+  constexpr int E = BL * kKC<V>;
   const ScanArgs& a = fa.s;
 #pragma unroll
   for (int k = 0; k < D; ++k) {
@@ -474,9 +503,9 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
       if (--st.kc == 0) {
         st.kc = a.K;
         if (st.ckv && t + 1 < T) {
-          store_vec<BL>(at(st.ckv, lo.c), st.vd);
+          store_vec<E>(at(st.ckv, lo.c), st.vd);
           if (lead) *at(st.ckh, lo.v) = st.h;
-          st.ckv += a.N * a.B;
+          st.ckv += a.N * a.P;
           st.ckh += a.N;
         }
       }
@@ -487,7 +516,7 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
   st.t += D;
   if (st.t >= Tp) {  // next batch item of this lane
     const int64_t n0 = (st.sp - static_cast<IO*>(fa.spikes)) - int64_t(T) * a.N + item_neurons;
-    fwd_item_start<IO, BL>(fa, n0, st);
+    fwd_item_start<IO, E>(fa, n0, st);
   }
 }
 
@@ -498,32 +527,33 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   const ScanArgs& a = fa.s;
   const Pos pos = locate<L>(a);
   if (!pos.active) return;  // whole L-lane groups leave together
-  Branches<BL> br;
-  load_branches<BL>(a, pos.c, pos.sub, br);
+  constexpr int E = BL * kKC<V>;
+  Branches<BL, kKC<V>> br;
+  load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br);
   const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-  const LaneOff lo = lane_offsets<IO, BL>(a, pos);
+  const LaneOff lo = lane_offsets<IO, E>(a, pos);
   const bool lead = pos.sub == 0;
   const int T = int(a.T);
   const int Tp = (T + D - 1) / D * D;
-  const int64_t rowX = a.N * a.B;
+  const int64_t rowX = a.N * a.P;
   int64_t bt0;
   const int nk = items_of(a, pos, &bt0);
   const int nchunks = nk * (Tp / D);
   const int64_t item_neurons = int64_t(a.ways) * a.M;
 
-  RowCursor<IO, BL, D> cur;
-  cur.base = static_cast<const IO*>(a.x) + bt0 * a.M * a.B;
+  RowCursor<IO, E, D> cur;
+  cur.base = static_cast<const IO*>(a.x) + bt0 * a.M * a.P;
   cur.k = 0;
   cur.t = 0;
-  FwdLane<IO, BL> st;
-  fwd_item_start<IO, BL>(fa, bt0 * a.M, st);
+  FwdLane<IO, E> st;
+  fwd_item_start<IO, E>(fa, bt0 * a.M, st);
 
-  float bufA[D][BL], bufB[D][BL];
-  if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
+  float bufA[D][E], bufB[D][E];
+  if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
   for (int c = 0; c < nchunks; c += 2) {
-    if (c + 1 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufB);
+    if (c + 1 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufB);
     compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
-    if (c + 2 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.B, bufA);
+    if (c + 2 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
     if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
   }
 }
@@ -537,17 +567,17 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
 // the dendritic state and H in registers, then runs the adjoint recurrences
 // backwards through them.
 // ---------------------------------------------------------------------------
-template <int BL>
+template <int BL, int E>
 struct Accum {
-  float k[BL], xi[BL], z[BL];
+  float k[BL], xi[E], z[BL];
   float a;   // g_alpha terms of this lane's branches
   float b;   // g_beta terms of this lane's neuron (counted by its first lane only)
 };
 
-template <typename IO, int BL>
+template <typename IO, int E>
 struct BwdLane {  // adjoint state carried backwards through time, and pointers
   float dh_next;
-  float lam[BL];
+  float lam[E];
   const IO* xbase;   // X of this batch item (uniform)
   IO* gxbase;
   const IO* gsbase;
@@ -555,18 +585,18 @@ struct BwdLane {  // adjoint state carried backwards through time, and pointers
 };
 
 // The streamed inputs of one chunk of CS steps.
-template <int BL, int CS>
+template <int E, int CS>
 struct ChunkIn {
-  float x[CS][BL];
+  float x[CS][E];
   float gs[CS];
   float gv[CS];
 };
 
 // grad_v_soma rows of a chunk (0 without grad_v_soma); issued with the chunk's
 // other loads so no step waits on a load issued after its stores.
-template <int BL, int CS>
+template <int E, int CS>
 __device__ __forceinline__ void load_chunk_gv(const ScanArgs& a, const LaneOff& lo, const float* gvbase, int c0,
-                                              ChunkIn<BL, CS>& in) {
+                                              ChunkIn<E, CS>& in) {
   if (gvbase) {
 #pragma unroll
     for (int k = 0; k < CS; ++k) in.gv[k] = __builtin_nontemporal_load(at(gvbase + int64_t(c0 + k) * a.N, lo.v));
@@ -576,37 +606,37 @@ __device__ __forceinline__ void load_chunk_gv(const ScanArgs& a, const LaneOff& 
   }
 }
 
-template <typename IO, int BL, int CS>
+template <typename IO, int E, int CS>
 __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
-                                              const IO* gsbase, const float* gvbase, int c0, ChunkIn<BL, CS>& in) {
-  const int64_t rowX = a.N * a.B;
+                                              const IO* gsbase, const float* gvbase, int c0, ChunkIn<E, CS>& in) {
+  const int64_t rowX = a.N * a.P;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
     const int64_t t = c0 + k;
-    load_vec<BL>(at(xbase + t * rowX, lo.x), in.x[k]);
+    load_vec<E>(at(xbase + t * rowX, lo.x), in.x[k]);
     in.gs[k] = load_one(at(gsbase + t * a.N, lo.s));
   }
-  load_chunk_gv<BL, CS>(a, lo, gvbase, c0, in);
+  load_chunk_gv<E, CS>(a, lo, gvbase, c0, in);
 }
 
 // The checkpointed state a segment starts from.
-template <int BL>
+template <int E>
 struct SegStart {
-  float v[BL];
+  float v[E];
   float h;
 };
 
-template <typename IO, int BL>
+template <typename IO, int E>
 __device__ __forceinline__ void load_seg_start(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int seg,
-                                               SegStart<BL>& st) {
+                                               SegStart<E>& st) {
   const ScanArgs& a = ba.s;
   if (seg == 0) {
 #pragma unroll
-    for (int j = 0; j < BL; ++j) st.v[j] = 0.0f;
+    for (int j = 0; j < E; ++j) st.v[j] = 0.0f;
     st.h = 0.0f;
   } else {
-    load_vec<BL>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.B, lo.c), st.v);
-    st.h = __builtin_nontemporal_load(at(ba.ckpt + int64_t(a.nck) * a.N * a.B + int64_t(seg - 1) * a.N + n0, lo.v));
+    load_vec<E>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.P, lo.c), st.v);
+    st.h = __builtin_nontemporal_load(at(ba.ckpt + int64_t(a.nck) * a.N * a.P + int64_t(seg - 1) * a.N + n0, lo.v));
   }
 }
 
@@ -615,7 +645,7 @@ __device__ __forceinline__ void load_seg_start(const BwdArgs& ba, const LaneOff&
 // exp(-u^2/2) factor of each step.
 template <int BL, int CS, int V>
 struct Stash {
-  float v[CS + 1][BL];
+  float v[CS + 1][BL * kKC<V>];
   float e[kMH<V> ? CS : 1][BL];
   float h[CS];
   float hd0;  // (1 - S) H before the chunk's first step: the decayed term beta multiplies
@@ -624,18 +654,19 @@ struct Stash {
 // Re-runs the chunk's forward steps exactly as the forward kernel did (the same
 // inline step function, so the same bits).
 template <int BL, int L, int V, int CS>
-__device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branches<BL>& br, float alpha,
-                                                const float (&v0)[BL], float h0, bool s0,
-                                                const float (&x)[CS][BL], Stash<BL, CS, V>& st) {
+__device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branches<BL, kKC<V>>& br, float alpha,
+                                                const float (&v0)[BL * kKC<V>], float h0, bool s0,
+                                                const float (&x)[CS][BL * kKC<V>], Stash<BL, CS, V>& st) {
+  constexpr int E = BL * kKC<V>;
 #pragma unroll
-  for (int j = 0; j < BL; ++j) st.v[0][j] = v0[j];
+  for (int j = 0; j < E; ++j) st.v[0][j] = v0[j];
   st.hd0 = s0 ? 0.0f : h0;
   float h = h0;
   bool s = s0;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
 #pragma unroll
-    for (int j = 0; j < BL; ++j) st.v[k + 1][j] = st.v[k][j];
+    for (int j = 0; j < E; ++j) st.v[k + 1][j] = st.v[k][j];
     const float z = dendrite_step<BL, L, V>(st.v[k + 1], x[k], br, alpha, kMH<V> ? st.e[kMH<V> ? k : 0] : nullptr);
     soma_step(h, s, z, a.beta, a.vth);
     st.h[k] = h;
@@ -645,12 +676,13 @@ __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branche
 // The adjoint recurrences through one chunk, last step first; writes grad_x
 // and accumulates the parameter gradients.
 template <typename IO, int BL, int L, int V, int CS>
-__device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
+__device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, float beta_r, int c0, const Stash<BL, CS, V>& st,
-                                              const float (&gs)[CS], const float (&gvr)[CS], BwdLane<IO, BL>& bl,
-                                              Accum<BL>& acc) {
+                                              const float (&gs)[CS], const float (&gvr)[CS],
+                                              BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
+  constexpr int KC = kKC<V>, E = BL * KC;
   const ScanArgs& a = ba.s;
-  const int64_t rowX = a.N * a.B;
+  const int64_t rowX = a.N * a.P;
   const float beta = a.beta, vth = a.vth;
 #pragma unroll
   for (int k = CS - 1; k >= 0; --k) {
@@ -663,38 +695,69 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
     // H[t] = beta (1 - S[t-1]) H[t-1] + Z[t]: learnable-beta (PLIF) gradient
     const float hd = k > 0 ? (st.h[k > 0 ? k - 1 : 0] >= vth ? 0.0f : st.h[k > 0 ? k - 1 : 0]) : st.hd0;
     acc.b = fmaf(dh, hd, acc.b);
-    float gxo[BL];
+    float gxo[E];
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
-      const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
-      float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
-      if constexpr (kMH<V>) {
-        const float q = tt * tt;
-        const float e = st.e[kMH<V> ? k : 0][j];
-        y = (1.0f - q) * e;
-        dps = tt * (q - 3.0f) * e;
+      if constexpr (KC == 1) {
+        const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
+        float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
+        if constexpr (kMH<V>) {
+          const float q = tt * tt;
+          const float e = st.e[kMH<V> ? k : 0][j];
+          y = (1.0f - q) * e;
+          dps = tt * (q - 3.0f) * e;
+        } else {
+          y = fabsf(tt);
+          dps = tt > 0.0f ? 1.0f : (tt < 0.0f ? -1.0f : 0.0f);
+        }
+        const float r = (br.k[j] * dh) * dps * br.rz[j];
+        bl.lam[j] = fmaf(alpha, bl.lam[j], r);
+        gxo[j] = kRes<V> ? fmaf(dh, br.rp, bl.lam[j]) : bl.lam[j];
+        acc.k[j] = fmaf(dh, y, acc.k[j]);
+        acc.xi[j] -= r;
+        acc.z[j] = fmaf(-r, tt, acc.z[j]);
+        acc.a = fmaf(bl.lam[j], st.v[k][j], acc.a);
       } else {
-        y = fabsf(tt);
-        dps = tt > 0.0f ? 1.0f : (tt < 0.0f ? -1.0f : 0.0f);
+        // u = ||d|| rz with d = Vd - xi over the branch's compartments;
+        // du/dVd_i = rz d_i / ||d|| (0 at ||d|| = 0), du/dzeta = -u rz.
+        const float nrm = __builtin_amdgcn_sqrtf(branch_sumsq<KC>(&st.v[k + 1][j * KC], &br.xi[j * KC]));
+        const float u = nrm * br.rz[j];
+        const float g = br.k[j] * dh;
+        float y, w, gzu;  // psi(u), the factor of d_i in dL/dVd_i, and psi'(u) u
+        if constexpr (kMH<V>) {
+          const float q = u * u;
+          const float e = st.e[kMH<V> ? k : 0][j];
+          y = (1.0f - q) * e;
+          const float qe = (q - 3.0f) * e;          // psi'(u) / u
+          w = g * qe * (br.rz[j] * br.rz[j]);        // g psi'(u) rz / ||d||
+          gzu = qe * q;
+        } else {
+          y = u;
+          w = nrm > 0.0f ? g * br.rz[j] * __builtin_amdgcn_rcpf(nrm) : 0.0f;
+          gzu = u;
+        }
+#pragma unroll
+        for (int i = j * KC; i < (j + 1) * KC; ++i) {
+          const float r = w * (st.v[k + 1][i] - br.xi[i]);
+          bl.lam[i] = fmaf(alpha, bl.lam[i], r);
+          gxo[i] = kRes<V> ? fmaf(dh, br.rp, bl.lam[i]) : bl.lam[i];
+          acc.xi[i] -= r;
+          acc.a = fmaf(bl.lam[i], st.v[k][i], acc.a);
+        }
+        acc.k[j] = fmaf(dh, y, acc.k[j]);
+        acc.z[j] = fmaf(-g * gzu, br.rz[j], acc.z[j]);
       }
-      const float r = (br.k[j] * dh) * dps * br.rz[j];
-      bl.lam[j] = fmaf(alpha, bl.lam[j], r);
-      gxo[j] = kRes<V> ? fmaf(dh, br.rp, bl.lam[j]) : bl.lam[j];
-      acc.k[j] = fmaf(dh, y, acc.k[j]);
-      acc.xi[j] -= r;
-      acc.z[j] = fmaf(-r, tt, acc.z[j]);
-      acc.a = fmaf(bl.lam[j], st.v[k][j], acc.a);
     }
-    store_vec_nt<BL>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
+    store_vec_nt<E>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
     bl.dh_next = dh;
   }
 }
 
 template <typename IO, int BL, int L, int V, int CS>
-__device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
-                                          float alpha, float beta_r, int c0, const float (&v0)[BL], float h0,
-                                          bool s0, const ChunkIn<BL, CS>& in, BwdLane<IO, BL>& bl,
-                                          Accum<BL>& acc) {
+__device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
+                                          float alpha, float beta_r, int c0, const float (&v0)[BL * kKC<V>],
+                                          float h0, bool s0, const ChunkIn<BL * kKC<V>, CS>& in,
+                                          BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
   Stash<BL, CS, V> st;
   recompute_chunk<BL, L, V, CS>(ba.s, br, alpha, v0, h0, s0, in.x, st);
   reverse_chunk<IO, BL, L, V, CS>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
@@ -702,13 +765,14 @@ __device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, 
 
 // Runs the forward from (vd, h, s) at step t_from up to (not including) t_to.
 template <typename IO, int BL, int L, int V>
-__device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, const Branches<BL>& br,
-                                        float alpha, const IO* xbase, int t_from, int t_to, float (&vd)[BL],
-                                        float& h, bool& s) {
-  const int64_t rowX = a.N * a.B;
+__device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
+                                        float alpha, const IO* xbase, int t_from, int t_to,
+                                        float (&vd)[BL * kKC<V>], float& h, bool& s) {
+  constexpr int E = BL * kKC<V>;
+  const int64_t rowX = a.N * a.P;
   for (int t = t_from; t < t_to; ++t) {
-    float xv[BL];
-    load_vec<BL>(at(xbase + int64_t(t) * rowX, lo.x), xv);
+    float xv[E];
+    load_vec<E>(at(xbase + int64_t(t) * rowX, lo.x), xv);
     const float z = dendrite_step<BL, L, V>(vd, xv, br, alpha);
     soma_step(h, s, z, a.beta, a.vth);
   }
@@ -716,14 +780,16 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
 
 // Loads a chunk of CS steps and runs it (used for every chunk but a prefetched one).
 template <typename IO, int BL, int L, int V, int CS>
-__device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
-                                                   float alpha, float beta_r, int t0, int c0, const SegStart<BL>& ss,
-                                                   BwdLane<IO, BL>& bl, Accum<BL>& acc) {
-  ChunkIn<BL, CS> in;
-  load_chunk_in<IO, BL, CS>(ba.s, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
-  float v[BL];
+__device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const LaneOff& lo,
+                                                   const Branches<BL, kKC<V>>& br, float alpha, float beta_r,
+                                                   int t0, int c0, const SegStart<BL * kKC<V>>& ss,
+                                                   BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
+  constexpr int E = BL * kKC<V>;
+  ChunkIn<E, CS> in;
+  load_chunk_in<IO, E, CS>(ba.s, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+  float v[E];
 #pragma unroll
-  for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
+  for (int j = 0; j < E; ++j) v[j] = ss.v[j];
   float h = ss.h;
   bool s = ss.h >= ba.s.vth && t0 > 0;
   advance<IO, BL, L, V>(ba.s, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
@@ -737,27 +803,29 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
 // is a multiple of KS, and only then is it prefetched.
 template <typename IO, int BL, int L, int V, int KS>
 __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff& lo, int64_t bt,
-                                                const Branches<BL>& br, float alpha, Accum<BL>& acc) {
+                                                const Branches<BL, kKC<V>>& br, float alpha,
+                                                Accum<BL, BL * kKC<V>>& acc) {
+  constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const int T = int(a.T);
   const int K = a.K;
   const float beta_r = ba.detach ? 0.0f : a.beta;
   const int64_t n0 = bt * a.M;  // first neuron of this batch item (wave-uniform)
-  BwdLane<IO, BL> bl;
-  bl.xbase = static_cast<const IO*>(a.x) + n0 * a.B;
-  bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.B;
+  BwdLane<IO, E> bl;
+  bl.xbase = static_cast<const IO*>(a.x) + n0 * a.P;
+  bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.P;
   bl.gsbase = static_cast<const IO*>(ba.gspk) + n0;
   bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
   bl.dh_next = 0.0f;
 #pragma unroll
-  for (int j = 0; j < BL; ++j) bl.lam[j] = 0.0f;
+  for (int j = 0; j < E; ++j) bl.lam[j] = 0.0f;
 
   const int nseg = (T + K - 1) / K;
   for (int seg = nseg - 1; seg >= 0; --seg) {
     const int t0 = seg * K;
     const int t1 = min(T, t0 + K);
-    SegStart<BL> ss;
-    load_seg_start<IO, BL>(ba, lo, n0, seg, ss);
+    SegStart<E> ss;
+    load_seg_start<IO, E>(ba, lo, n0, seg, ss);
     // Chunks: the remainder (len mod KS) first, in descending powers of two
     // from t0, then whole KS-step chunks; visited from the last one back.  A
     // chunk re-runs the forward from t0 up to its first step, so putting the
@@ -767,11 +835,11 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
     const int rem = len - nfull * KS;
     for (int ch = nfull - 1; ch >= 0; --ch) {
       const int c0 = t0 + rem + ch * KS;
-      ChunkIn<BL, KS> in;
-      load_chunk_in<IO, BL, KS>(a, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
-      float v[BL];
+      ChunkIn<E, KS> in;
+      load_chunk_in<IO, E, KS>(a, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+      float v[E];
 #pragma unroll
-      for (int j = 0; j < BL; ++j) v[j] = ss.v[j];
+      for (int j = 0; j < E; ++j) v[j] = ss.v[j];
       float h = ss.h;
       bool s = ss.h >= a.vth && t0 > 0;
       advance<IO, BL, L, V>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
@@ -799,57 +867,89 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
 // the registers of its own rows are free again, so they stream in while the
 // adjoint pass runs.
 template <typename IO, int BL, int L, int V, int KS>
-__device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo, const Branches<BL>& br,
-                                                   float alpha, int64_t bt0, int nk, Accum<BL>& acc) {
+__device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo,
+                                                   const Branches<BL, kKC<V>>& br, float alpha, int64_t bt0,
+                                                   int nk, Accum<BL, BL * kKC<V>>& acc) {
+  constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const float beta_r = ba.detach ? 0.0f : a.beta;
   const int64_t step = int64_t(a.ways) * a.M;  // neurons between this lane's items
   int64_t n0 = bt0 * a.M;
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
-  ChunkIn<BL, KS> cur;
-  if (nk > 0) load_chunk_in<IO, BL, KS>(a, lo, x + n0 * a.B, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
-  float zero[BL];
+  ChunkIn<E, KS> cur;
+  if (nk > 0) load_chunk_in<IO, E, KS>(a, lo, x + n0 * a.P, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
+  float zero[E];
 #pragma unroll
-  for (int j = 0; j < BL; ++j) zero[j] = 0.0f;
+  for (int j = 0; j < E; ++j) zero[j] = 0.0f;
   for (int i = 0; i < nk; ++i) {
-    BwdLane<IO, BL> bl;
-    bl.xbase = x + n0 * a.B;
-    bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.B;
+    BwdLane<IO, E> bl;
+    bl.xbase = x + n0 * a.P;
+    bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.P;
     bl.gsbase = g + n0;
     bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
     bl.dh_next = 0.0f;
 #pragma unroll
-    for (int j = 0; j < BL; ++j) bl.lam[j] = 0.0f;
+    for (int j = 0; j < E; ++j) bl.lam[j] = 0.0f;
     Stash<BL, KS, V> st;
     recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
-    ChunkIn<BL, KS> nxt;
+    ChunkIn<E, KS> nxt;
     const int64_t n1 = n0 + step;
-    if (i + 1 < nk) load_chunk_in<IO, BL, KS>(a, lo, x + n1 * a.B, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
+    if (i + 1 < nk) load_chunk_in<IO, E, KS>(a, lo, x + n1 * a.P, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
     reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
     cur = nxt;
     n0 = n1;
   }
 }
 
-// Where partial slot p of output (c, q, b) lives in the workspace: output-major
-// ([3CB][P], read by one wave per output) when there are many slots, slot-major
-// ([P][3CB], read by one thread per output) when there are few.
-__device__ __forceinline__ int64_t partial_index(const BwdArgs& ba, int64_t c, int q, int b, int64_t p) {
-  const int64_t o = (c * 3 + q) * ba.s.B + b;
-  return ba.wide ? o * ba.P + p : p * (3 * ba.s.C * ba.s.B) + o;
+// Per channel the backward produces W = 2 B + P parameter gradients, in the
+// order g_kappa [B], g_xi [P], g_zeta [B].  Partial slot p of output o of
+// channel c lives output-major ([C W][slots], read by one wave per output) when
+// there are many slots, slot-major ([slots][C W], one thread per output) when
+// there are few.
+__device__ __forceinline__ int64_t partial_index(const BwdArgs& ba, int64_t c, int o, int64_t p) {
+  const int W = 2 * ba.s.B + ba.s.P;
+  const int64_t g = c * W + o;
+  return ba.wide ? g * ba.slots + p : p * (ba.s.C * W) + g;
+}
+
+// A lane's NV = 2 BL + E accumulators, v = 0 .. NV-1: g_kappa of its BL
+// branches, g_xi of its E compartments, g_zeta of its branches.
+template <int BL, int E>
+__device__ __forceinline__ float accum_value(const Accum<BL, E>& acc, int v) {
+  float r = 0.0f;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) r = v == j ? acc.k[j] : r;
+#pragma unroll
+  for (int i = 0; i < E; ++i) r = v == BL + i ? acc.xi[i] : r;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) r = v == BL + E + j ? acc.z[j] : r;
+  return r;
+}
+
+// Channel output o (0 .. W-1) -> (lane-in-neuron sub, accumulator index v).
+template <int BL, int E>
+__device__ __forceinline__ void output_source(int o, int B, int P, int* sub, int* v) {
+  if (o < B) {
+    *sub = o / BL; *v = o % BL;
+  } else if (o < B + P) {
+    *sub = (o - B) / E; *v = BL + (o - B) % E;
+  } else {
+    *sub = (o - B - P) / BL; *v = BL + E + (o - B - P) % BL;
+  }
 }
 
 // Block reduction of the parameter-gradient partials, in a fixed order.
-template <int BL, int L>
-__device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& pos, Accum<BL>& acc) {
+template <int BL, int E, int L>
+__device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& pos, Accum<BL, E>& acc) {
+  constexpr int NV = 2 * BL + E;
   const ScanArgs& a = ba.s;
-  __shared__ float red[kThreads * BL];
+  __shared__ float red[kThreads * E];
   __shared__ float reda[kThreads / 64];
   __shared__ float redb[kThreads / 64];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int B = a.B;
+  const int B = a.B, P = a.P, W = 2 * B + P;
 
   float va = acc.a, vb = acc.b;
 #pragma unroll
@@ -867,42 +967,44 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
     const int64_t c = pos.c;
     const int64_t jt = pos.tile % a.tpc;
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
+    for (int v = 0; v < NV; ++v) {
+      float x = accum_value(acc, v);
 #pragma unroll
-      for (int j = 0; j < BL; ++j) {
-        float v = q == 0 ? acc.k[j] : (q == 1 ? acc.xi[j] : acc.z[j]);
-#pragma unroll
-        for (int off = 32; off >= L; off >>= 1) v += __shfl_xor(v, off);
-        if (lane < L) red[((q * BL + j) * 4 + wave) * L + lane] = v;
-      }
+      for (int off = 32; off >= L; off >>= 1) x += __shfl_xor(x, off);
+      if (lane < L) red[(v * 4 + wave) * L + lane] = x;
     }
     __syncthreads();
-    for (int o = tid; o < 3 * B; o += kThreads) {
-      const int q = o / B, b = o % B;
-      const int sub = b / BL, j = b % BL;
-      float s = 0.0f;
-      for (int w = 0; w < 4; ++w) s += red[((q * BL + j) * 4 + w) * L + sub];
-      ba.wsP[partial_index(ba, c, q, b, int64_t(pos.g) * a.tpc + jt)] = s;
+    for (int o = tid; o < W; o += kThreads) {
+      int sub, v;
+      output_source<BL, E>(o, B, P, &sub, &v);
+      float sum = 0.0f;
+      for (int w = 0; w < 4; ++w) sum += red[(v * 4 + w) * L + sub];
+      ba.wsP[partial_index(ba, c, o, int64_t(pos.g) * a.tpc + jt)] = sum;
     }
   } else {
-    // Whole channels per tile: sum the batch ways and the S positions of each channel.
+    // Whole channels per tile: sum the batch ways and the S positions of each
+    // channel, one accumulator kind (kappa, xi, zeta) at a time.
     for (int q = 0; q < 3; ++q) {
+      const int nq = q == 1 ? E : BL;         // accumulators of this kind per lane
+      const int v0 = q == 0 ? 0 : (q == 1 ? BL : BL + E);
+      const int o0 = q == 0 ? 0 : (q == 1 ? B : B + P);
+      const int wq = q == 1 ? P : B;          // outputs of this kind per channel
 #pragma unroll
-      for (int j = 0; j < BL; ++j)
-        red[tid * BL + j] = q == 0 ? acc.k[j] : (q == 1 ? acc.xi[j] : acc.z[j]);
+      for (int j = 0; j < E; ++j)
+        if (j < nq) red[tid * E + j] = accum_value(acc, v0 + j);
       __syncthreads();
-      for (int o = tid; o < a.cpt * B; o += kThreads) {
-        const int slot = o / B, b = o % B;
+      for (int o = tid; o < a.cpt * wq; o += kThreads) {
+        const int slot = o / wq, ol = o % wq;
         const int64_t c = pos.tile * a.cpt + slot;
         if (c >= a.C) continue;
-        const int sub = b / BL, j = b % BL;
-        float s = 0.0f;
+        const int sub = ol / nq, j = ol % nq;
+        float sum = 0.0f;
         for (int w = 0; w < a.ways; ++w)
           for (int sp = 0; sp < a.S; ++sp) {
             const int thr = (w * a.pb + slot * int(a.S) + sp) * L + sub;
-            s += red[thr * BL + j];
+            sum += red[thr * E + j];
           }
-        ba.wsP[partial_index(ba, c, q, b, pos.g)] = s;
+        ba.wsP[partial_index(ba, c, o0 + ol, pos.g)] = sum;
       }
       __syncthreads();
     }
@@ -915,20 +1017,23 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
 }
 
 template <typename IO, int BL, int L, int V, int KS>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * KS <= 8 ? 4 : (BL * KS <= 16 ? 3 : 2)))) dendsn_bwd_kernel(BwdArgs ba) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * kKC<V> * KS <= 8 ? 4 : (BL * kKC<V> * KS <= 16 ? 3 : 2)))) dendsn_bwd_kernel(BwdArgs ba) {
+  constexpr int E = BL * kKC<V>;
   if (ba.s.beta_p) ba.s.beta = ba.s.beta_p[0];  // learnable (PLIF) decay
   const ScanArgs& a = ba.s;
   const Pos pos = locate<L>(a);
-  Accum<BL> acc;
+  Accum<BL, E> acc;
 #pragma unroll
-  for (int j = 0; j < BL; ++j) acc.k[j] = acc.xi[j] = acc.z[j] = 0.0f;
+  for (int j = 0; j < BL; ++j) acc.k[j] = acc.z[j] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < E; ++i) acc.xi[i] = 0.0f;
   acc.a = 0.0f;
   acc.b = 0.0f;
   if (pos.active) {
-    Branches<BL> br;
-    load_branches<BL>(a, pos.c, pos.sub, br);
+    Branches<BL, kKC<V>> br;
+    load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br);
     const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-    const LaneOff lo = lane_offsets<IO, BL>(a, pos);
+    const LaneOff lo = lane_offsets<IO, E>(a, pos);
     int64_t bt0;
     const int nk = items_of(a, pos, &bt0);
     const int T = int(a.T);
@@ -946,7 +1051,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
   }
   if (pos.sub != 0) acc.b = 0.0f;  // the soma runs in every lane of a neuron: count it once
   // every thread of the block reaches this one call (it holds block barriers)
-  reduce_partials<BL, L>(ba, pos, acc);
+  reduce_partials<BL, E, L>(ba, pos, acc);
 }
 
 // Fixed-order float64 sum of the partials into the parameter gradients; the

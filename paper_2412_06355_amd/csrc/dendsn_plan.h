@@ -20,6 +20,7 @@ enum TileMode : int32_t {
 struct Plan {
   int32_t BL;     // branches held by one lane
   int32_t L;      // lanes per neuron (power of two, <= 16); B = BL * L
+  int32_t KC;     // compartments per branch (1, 2 or 4); a lane holds BL * KC of them
   int32_t fast;   // 1: a vector-width mapping with every stash capacity compiled
   int32_t mode;   // TileMode
   int32_t ways;   // batch ways inside a block (waves that share positions)
@@ -42,7 +43,7 @@ struct ScanArgs {
   const uint8_t* mask;  // NULL: all branches kept
   const float* beta_p;  // learnable somatic decay on the device, or NULL: beta
   int64_t T, N, C, S, M, batch;  // M = C * S positions per sample
-  int32_t B, K, nck;
+  int32_t B, P, K, nck;          // P = B * KC compartments: the innermost extent of X
   float beta, vth;
   float rP;             // 1 / P (residual dendrite)
   int32_t mode, ways, pb, tpc, cpt, bpg;
@@ -62,11 +63,11 @@ struct BwdArgs {
   const void* gspk;
   const float* gv;  // optional
   void* gx;
-  float* wsP;       // partial sums of (g_kappa, g_xi, g_zeta): P slots per output, see partial_index
+  float* wsP;       // partial sums of (g_kappa, g_xi, g_zeta): `slots` per output, see partial_index
   float* wsA;       // [G][ntiles] partial sums of g_alpha
   float* wsB;       // [G][ntiles] partial sums of g_beta
-  int64_t P;        // partial slots per output: G * tpc
-  int32_t wide;     // 1: output-major layout (P > kNarrowSlots)
+  int64_t slots;    // partial slots per output: G * tpc
+  int32_t wide;     // 1: output-major layout (slots > kNarrowSlots)
   int32_t detach;
   int32_t sg;
   float sg_scale;
@@ -82,18 +83,30 @@ struct FinArgs {
   float* gxi;
   float* gz;
   float* ga;
-  int64_t C, nA, P;
-  int32_t B, wide, stateful;
+  int64_t C, nA, slots;
+  int32_t B, P, KC, wide, stateful;
 };
 
 constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread per output
 
-// Compiled (BL, L) mappings.  "Fast" mappings move 8 or 16 bytes per lane;
-// "generic" ones cover other branch counts.  Backward stash capacities: 4 steps
-// for every mapping, and 8 steps too when a lane holds at most 4 branches.
+// Compiled (BL, L) mappings with one compartment per branch.  "Fast" mappings
+// move 8 or 16 bytes per lane; "generic" ones cover other branch counts.
+// Backward stash capacities: 4 steps for every mapping, and 8 steps too when a
+// lane holds at most 4 branches.
 #define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
 #define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
 #define DENDSN_GENERIC(X) X(1, 1) X(2, 1) X(3, 1) X(5, 1) X(6, 1) X(7, 1) X(5, 2) X(6, 2) X(7, 2)
 #define DENDSN_GENERIC_KS 4
+
+// Compiled (BL, L, KC) mappings with KC = 2 or 4 compartments per branch (stash
+// capacity 4).  Fast ones put 16 bytes of compartments in a lane (BL KC = 4
+// for fp32, 8 for bf16); generic ones hold a whole neuron of up to 14
+// compartments in one lane.
+#define DENDSN_KC_FAST_F32(X) X(2, 1, 2) X(2, 2, 2) X(2, 4, 2) X(2, 8, 2) X(2, 16, 2) \
+                              X(1, 1, 4) X(1, 2, 4) X(1, 4, 4) X(1, 8, 4) X(1, 16, 4)
+#define DENDSN_KC_FAST_BF16(X) X(4, 1, 2) X(4, 2, 2) X(4, 4, 2) X(4, 8, 2) X(4, 16, 2) \
+                               X(2, 1, 4) X(2, 2, 4) X(2, 4, 4) X(2, 8, 4) X(2, 16, 4)
+#define DENDSN_KC_GENERIC(X) X(1, 1, 2) X(2, 1, 2) X(3, 1, 2) X(5, 1, 2) X(6, 1, 2) X(7, 1, 2) \
+                             X(1, 1, 4) X(2, 1, 4) X(3, 1, 4)
 
 }  // namespace dendsn

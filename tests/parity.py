@@ -87,15 +87,15 @@ def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True,
     import torch
 
     rng = np.random.default_rng(seed)
-    T, N, B, C = cfg.T, cfg.N, cfg.B, cfg.C
-    X = rng.normal(x_mean, x_std, size=(T, N, B)).astype(np.float32)
+    T, N, B, C, P = cfg.T, cfg.N, cfg.B, cfg.C, cfg.P
+    X = rng.normal(x_mean, x_std, size=(T, N, P)).astype(np.float32)
     gS = rng.normal(size=(T, N)).astype(np.float32)
     if cfg.io == "bf16":
         X = torch.from_numpy(X).to(torch.bfloat16).float().numpy()
         gS = torch.from_numpy(gS).to(torch.bfloat16).float().numpy()
     kappa = rng.uniform(0.0, 1.0, size=(C, B)).astype(np.float32)
     if random_affine:
-        xi = rng.normal(0.0, 0.5, size=(C, B)).astype(np.float32)
+        xi = rng.normal(0.0, 0.5, size=(C, P)).astype(np.float32)
         zeta = rng.uniform(0.5, 2.0, size=(C, B)).astype(np.float32)
     else:
         xi = zeta = None
@@ -151,7 +151,8 @@ def run_oracle(case: Case, force=None):
     rec = oracle.forward(
         case.X.astype(np.float64), alpha=case.alpha if cfg.stateful else 0.0, beta=case.beta, v_th=cfg.v_th,
         kappa=case.kappa, xi=case.xi, zeta=case.zeta, mask=case.mask, C=cfg.C, S=cfg.S,
-        psi_kind=cfg.psi, stateful=cfg.stateful, residual=cfg.residual, force=force)
+        psi_kind=cfg.psi, stateful=cfg.stateful, residual=cfg.residual,
+        comps_per_branch=cfg.comps_per_branch, force=force)
     return rec
 
 
@@ -254,11 +255,13 @@ def compare(case: Case, gpu: dict) -> Report:
     close_summed("g_beta", gpu["g_beta"], og["g_beta"], og["abs_beta"], RTOL_F32, gr, rep)
     if case.mask is not None:
         off = case.mask == 0
-        for k in ("g_kappa", "g_xi", "g_zeta"):
+        off_c = np.repeat(off, cfg.comps_per_branch, axis=1)   # per compartment
+        for k in ("g_kappa", "g_zeta"):
             assert np.all(gpu[k][off] == 0.0), k
+        assert np.all(gpu["g_xi"][off_c] == 0.0)
         if not cfg.residual:
             # a gated-off branch feeds nothing to the soma; with the residual
             # dendrite its input still reaches the soma through the mean
             cidx = (np.arange(cfg.N) // cfg.S) % cfg.C
-            assert np.all(gpu["gX"][:, off[cidx]] == 0.0)
+            assert np.all(gpu["gX"][:, off_c[cidx]] == 0.0)
     return rep

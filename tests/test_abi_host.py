@@ -77,12 +77,13 @@ def test_status_strings(lib):
         assert dendsn.dendsn_status_str(code) == name
 
 
-@pytest.mark.parametrize("T,K,batch,C,S,B", [(4, 4, 2, 256, 1, 4), (64, 8, 32, 4096, 1, 16),
-                                             (10, 3, 3, 5, 7, 6), (7, 100, 1, 1, 1, 1)])
-def test_ckpt_bytes(lib, T, K, batch, C, S, B):
-    cfg = dendsn.DendSNConfig(T=T, batch=batch, C=C, S=S, B=B, ckpt_every=K)
+@pytest.mark.parametrize("T,K,batch,C,S,B,k", [(4, 4, 2, 256, 1, 4, 1), (64, 8, 32, 4096, 1, 16, 1),
+                                               (10, 3, 3, 5, 7, 6, 1), (7, 100, 1, 1, 1, 1, 1),
+                                               (9, 2, 2, 3, 5, 2, 2), (9, 4, 2, 3, 1, 5, 2), (6, 5, 1, 2, 3, 3, 4)])
+def test_ckpt_bytes(lib, T, K, batch, C, S, B, k):
+    cfg = dendsn.DendSNConfig(T=T, batch=batch, C=C, S=S, B=B, ckpt_every=K, comps_per_branch=k)
     nck = -(-T // K) - 1
-    assert dendsn.dendsn_ckpt_bytes(cfg) == nck * batch * C * S * (B + 1) * 4
+    assert dendsn.dendsn_ckpt_bytes(cfg) == nck * batch * C * S * (B * k + 1) * 4
 
 
 def test_workspace_bytes_positive_and_grows_with_groups(lib):
@@ -95,7 +96,9 @@ def test_workspace_bytes_positive_and_grows_with_groups(lib):
 @pytest.mark.parametrize("kw,code", [
     (dict(T=0), E_INVALID), (dict(batch=0), E_INVALID), (dict(C=0), E_INVALID), (dict(S=0), E_INVALID),
     (dict(B=0), E_INVALID), (dict(B=129), E_INVALID), (dict(comps_per_branch=0), E_INVALID),
-    (dict(comps_per_branch=2), E_UNSUPPORTED), (dict(B=9), E_UNSUPPORTED), (dict(B=11), E_UNSUPPORTED),
+    (dict(comps_per_branch=3), E_UNSUPPORTED), (dict(comps_per_branch=8), E_UNSUPPORTED),
+    (dict(B=12, comps_per_branch=2), E_UNSUPPORTED), (dict(B=5, comps_per_branch=4), E_UNSUPPORTED),
+    (dict(B=9), E_UNSUPPORTED), (dict(B=11), E_UNSUPPORTED),
     (dict(stateful=2), E_INVALID), (dict(detach_reset=-1), E_INVALID), (dict(ckpt_every=0), E_INVALID),
     (dict(io=2), E_INVALID), (dict(psi=5), E_INVALID), (dict(sg=3), E_INVALID),
     (dict(sg_scale=0.0), E_INVALID), (dict(sg_scale=float("nan")), E_INVALID),
@@ -168,7 +171,19 @@ def test_supported_branch_counts(lib):
 
 
 def test_python_binding_raises_on_error():
-    cfg = dendsn.DendSNConfig(T=4, batch=2, C=4, S=1, B=4, comps_per_branch=2)
+    cfg = dendsn.DendSNConfig(T=4, batch=2, C=4, S=1, B=4, comps_per_branch=3)
     with pytest.raises(dendsn.DendSNError) as e:
         dendsn.dendsn_ckpt_bytes(cfg)
     assert e.value.status == E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("io", [0, 1])
+@pytest.mark.parametrize("B,k", [(1, 2), (2, 2), (3, 2), (4, 2), (5, 2), (6, 2), (7, 2), (8, 2), (16, 2), (32, 2),
+                                 (1, 4), (2, 4), (3, 4), (4, 4), (8, 4), (16, 4)])
+def test_supported_compartment_layouts(lib, io, B, k):
+    """The host checks accept these branch counts with k compartments per branch
+    (the GPU parity tests launch each of their kernels)."""
+    cfg = base_cfg(B=B, comps_per_branch=k, io=io)
+    out = ctypes.c_size_t(0)
+    assert lib.dendsn_bwd_workspace_bytes(ctypes.byref(cfg), ctypes.byref(out)) == OK
+    assert out.value > 0

@@ -83,6 +83,75 @@ def test_shapes(gpu_device, shape, variant):
     compare(case, run_gpu(case, gpu_device))
 
 
+# --- several compartments per branch (L2 norm over a branch's compartments) ---
+KC_SHAPES = [
+    # T, batch, C, S, B, k, io, K
+    (4, 2, 5, 300, 2, 2, "f32", 4),      # fast fp32, one lane per neuron, conv tiles
+    (6, 3, 70, 1, 8, 2, "f32", 3),       # fast fp32, 4 lanes per neuron, FC tiles
+    (5, 2, 9, 7, 1, 4, "f32", 5),        # fast fp32, k = 4
+    (7, 2, 6, 33, 4, 4, "f32", 2),       # fast fp32, k = 4, 4 lanes
+    (4, 3, 4, 257, 4, 2, "bf16", 4),     # fast bf16
+    (9, 2, 5, 1, 16, 2, "bf16", 4),      # fast bf16, 4 lanes
+    (4, 2, 7, 65, 2, 4, "bf16", 4),      # fast bf16, k = 4
+    (4, 2, 6, 40, 5, 2, "f32", 4),       # generic: P = 10, B = 5
+    (10, 2, 3, 5, 3, 2, "f32", 4),       # generic, checkpoints
+    (4, 2, 5, 1, 7, 2, "f32", 4),        # generic, 14 compartments in a lane
+    (5, 2, 4, 9, 3, 4, "f32", 5),        # generic, k = 4
+    (4, 2, 6, 130, 2, 2, "bf16", 4),     # generic bf16
+    (6, 3, 4, 3, 1, 4, "bf16", 6),       # generic bf16, k = 4
+    (3, 2, 5, 17, 1, 2, "f32", 3),       # generic, one branch
+]
+
+
+@pytest.mark.parametrize("shape", KC_SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}k{}{}K{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "id-atan-stateless-res", "mh-atan-detach-plif-res"])
+def test_compartments_per_branch(gpu_device, shape, variant):
+    T, batch, C, S, B, k, io, K = shape
+    psi = "identity" if "-id-" in f"-{variant}-" else "mexhat"
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, comps_per_branch=k, io=io, ckpt_every=K, psi=psi,
+            sg="sigmoid" if "sig" in variant else "atan", stateful="stateless" not in variant,
+            detach_reset="detach" in variant, residual="res" in variant, beta=0.7)
+    seed = zlib.crc32(repr((shape, variant)).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6, mask_rho=0.5 if "mask" in variant else None,
+                     name=f"kc/{shape}/{variant}", beta_dev=0.8 if "plif" in variant else None)
+    compare(case, run_gpu(case, gpu_device))
+
+
+def test_compartments_checkpoint_interval_is_bit_invariant(gpu_device):
+    import torch
+
+    base = cfg(T=24, batch=2, C=40, S=1, B=8, comps_per_branch=2, beta=0.9, ckpt_every=8)
+    case = make_case(base, seed=23, x_mean=0.1, alpha=0.8, mask_rho=0.7, name="kc-ckpt")
+    d = to_device(case, gpu_device)
+    outs = []
+    for K in (8, 24, 5):
+        case.cfg = base.with_(ckpt_every=K)
+        outs.append(run_gpu(case, gpu_device, dev=d)["raw"])
+    for o in outs[1:]:
+        assert torch.equal(o["spikes"], outs[0]["spikes"])
+        assert torch.equal(_bits(o["grads"]["grad_x"]), _bits(outs[0]["grads"]["grad_x"]))
+    compare(case, run_gpu(case, gpu_device, dev=d))
+
+
+def test_replicated_compartments_match_one_compartment(gpu_device):
+    """k equal compartments (same input and xi) act as one with zeta / sqrt(k): spikes
+    agree and each copy gets 1/k of the one-compartment input gradient."""
+    k = 4
+    one = cfg(T=4, batch=2, C=16, S=64, B=2, psi="identity")
+    c1 = make_case(one, seed=24, random_affine=True, name="kc-rep/one")
+    ck = make_case(one.with_(comps_per_branch=k), seed=24, name="kc-rep/k")
+    ck.X = np.repeat(c1.X, k, axis=2)
+    ck.xi = np.repeat(c1.xi, k, axis=1)
+    ck.zeta = c1.zeta.copy()
+    ck.kappa, ck.gS = c1.kappa, c1.gS
+    c1.zeta = (c1.zeta / 2.0).astype(np.float32)   # sqrt(4) = 2, exact
+    g1, gk = run_gpu(c1, gpu_device), run_gpu(ck, gpu_device)
+    compare(c1, g1)
+    compare(ck, gk)
+    near = np.abs(g1["H"] - 1.0) < 1e-5
+    assert np.all((g1["S"] == gk["S"]) | near)
+
+
 # --- residual dendrite (ResStateful / ResStateless) and the PLIF soma ---
 @pytest.mark.parametrize("stateful", [True, False])
 @pytest.mark.parametrize("plif", [False, True])
