@@ -64,14 +64,15 @@ def _oracle_chunk(args):
 
     import oracle
 
-    (T, C, S, B, x_mean, x_std, alpha, beta, vth, psi, sg, sg_scale, seed) = args
+    (T, C, S, B, k, x_mean, x_std, alpha, beta, vth, psi, sg, sg_scale, stateful, residual, seed) = args
     rng = np.random.default_rng(seed)
     N = C * S
-    X = rng.normal(x_mean, x_std, size=(T, N, B))
+    X = rng.normal(x_mean, x_std, size=(T, N, B * k))
     gS = rng.normal(size=(T, N))
     kappa = rng.uniform(0.0, 1.0, size=(C, B))
     t0 = time.perf_counter()
-    rec = oracle.forward(X, alpha=alpha, beta=beta, v_th=vth, kappa=kappa, C=C, S=S, psi_kind=psi)
+    rec = oracle.forward(X, alpha=alpha if stateful else 0.0, beta=beta, v_th=vth, kappa=kappa, C=C, S=S,
+                         psi_kind=psi, stateful=stateful, residual=residual, comps_per_branch=k)
     oracle.backward(rec, gS, sg_kind=sg, sg_scale=sg_scale)
     return time.perf_counter() - t0, T * N * B
 
@@ -88,11 +89,11 @@ def cpu_baseline(wl, target_nbs: float):
     """Oracle fwd+bwd throughput on a bounded sample: whole batch items of the
     layer (about target_nbs neuron-branch-steps), one task per item, spread
     over a process pool of up to 16 host cores; timed after the pool is up."""
-    per_item = wl.T * wl.C * wl.S * wl.B
+    per_item = wl.T * wl.C * wl.S * wl.P
     items = int(max(1, min(wl.batch, round(target_nbs / per_item))))
     workers = int(min(16, len(os.sched_getaffinity(0)), items))
-    args = [(wl.T, wl.C, wl.S, wl.B, wl.x_mean, wl.x_std, wl.alpha, wl.beta, wl.v_th, wl.psi, wl.sg,
-             wl.sg_scale, 1000 + i) for i in range(items)]
+    args = [(wl.T, wl.C, wl.S, wl.B, wl.comps_per_branch, wl.x_mean, wl.x_std, wl.alpha, wl.beta, wl.v_th,
+             wl.psi, wl.sg, wl.sg_scale, wl.stateful, wl.residual, 1000 + i) for i in range(items)]
     with mp.get_context("spawn").Pool(workers) as pool:
         pool.map(_warm, range(workers))
         t0 = time.perf_counter()
@@ -105,7 +106,8 @@ def cpu_baseline(wl, target_nbs: float):
         "unit": "neuron-branch-steps/s",
         "cores": workers,
         "kind": "oracle",
-        "sample": f"{items} of {wl.batch} batch items of the layer (T={wl.T}, C={wl.C}, S={wl.S}, B={wl.B}), "
+        "sample": f"{items} of {wl.batch} batch items of the layer (T={wl.T}, C={wl.C}, S={wl.S}, B={wl.B}, "
+                  f"P={wl.P}), "
                   f"{nbs} neuron-branch-steps, float64 numpy forward+backward, one task per item on "
                   f"{workers} processes; {cpu_s:.1f} CPU-s in {wall:.2f} s wall",
     }
@@ -152,7 +154,8 @@ def main():
     cfg = dendsn.DendSNConfig(T=wl.T, batch=wl.batch, C=wl.C, S=wl.S, B=wl.B, stateful=wl.stateful,
                               detach_reset=wl.detach_reset, ckpt_every=wl.ckpt_every, io=wl.io, psi=wl.psi,
                               sg=wl.sg, sg_scale=wl.sg_scale, beta=wl.beta, v_th=wl.v_th,
-                              batch_groups=args.batch_groups)
+                              batch_groups=args.batch_groups, comps_per_branch=wl.comps_per_branch,
+                              residual=wl.residual)
     X, gS = workloads.activations(wl, device=dev, seed=0)
     p = workloads.params(wl, seed=0)
     kappa = torch.from_numpy(p["kappa"]).to(dev)
@@ -169,7 +172,7 @@ def main():
     g_alpha = torch.empty((1,), dtype=torch.float32, device=dev)
     g_beta = torch.empty((1,), dtype=torch.float32, device=dev)
     g_kappa = torch.empty_like(kappa)
-    g_xi = torch.empty_like(kappa)
+    g_xi = torch.empty((wl.C, wl.P), dtype=torch.float32, device=dev)
     g_zeta = torch.empty_like(kappa)
     ws = torch.empty(((dendsn.dendsn_bwd_workspace_bytes(cfg) + 3) // 4,), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
@@ -221,9 +224,10 @@ def main():
 
     esz = X.element_size()
     nbs = wl.T * wl.N * wl.B
+    ncs = wl.T * wl.N * wl.P                                        # compartment-steps: elements of X
     ck = nck_bytes
-    fwd_bytes = nbs * esz + wl.T * wl.N * esz + ck                  # read X, write S, write checkpoints
-    bwd_bytes = 2 * nbs * esz + wl.T * wl.N * esz + ck              # read X and gS, write gX, read checkpoints
+    fwd_bytes = ncs * esz + wl.T * wl.N * esz + ck                  # read X, write S, write checkpoints
+    bwd_bytes = 2 * ncs * esz + wl.T * wl.N * esz + ck              # read X and gS, write gX, read checkpoints
     digest = kernel_source_digest()
     traffic = measured_traffic(digest, wl.name)
     bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
@@ -245,7 +249,8 @@ def main():
         "dtype": "f32" if wl.io == "f32" else "bf16 storage, f32 arithmetic",
         "data": "synthetic",
         "config": {"workload": wl.name, "T": wl.T, "batch": wl.batch, "C": wl.C, "S": wl.S, "B": wl.B,
-                   "N": wl.N, "io": wl.io, "psi": wl.psi, "surrogate": f"{wl.sg}({wl.sg_scale})",
+                   "P": wl.P, "N": wl.N, "io": wl.io, "psi": wl.psi, "surrogate": f"{wl.sg}({wl.sg_scale})",
+                   "dendrite": ("res" if wl.residual else "") + ("stateful" if wl.stateful else "stateless"),
                    "alpha": wl.alpha, "beta": wl.beta, "v_th": wl.v_th, "ckpt_every": wl.K,
                    "tasks": n_tasks},
         "roofline": {"bound": "hbm", "kernel": "dendsn_backward (scan + finalize)",

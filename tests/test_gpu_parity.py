@@ -199,6 +199,10 @@ REDUCED = {
     "long_horizon_res_plif": dict(T=64, batch=2, C=4096, S=1, B=16, x_mean=0.1, alpha=0.8, beta=0.9,
                                   ckpt_every=8, residual=True, beta_dev=0.9),
     "cifar_res": dict(T=4, batch=2, C=128, S=1024, B=8, x_std=0.5, residual=True),
+    "cifar_p4b2": dict(T=4, batch=2, C=128, S=1024, B=2, comps_per_branch=2, x_std=0.5),
+    "tiny_imagenet_res": dict(T=4, batch=1, C=64, S=4096, B=2, comps_per_branch=2, psi="identity",
+                              stateful=False, residual=True),
+    "dvs_p10b5": dict(T=10, batch=1, C=128, S=1024, B=5, comps_per_branch=2, stateful=False),
 }
 
 

@@ -11,9 +11,11 @@ ImageNet-sized stem, a long-horizon fully connected layer, the task-incremental
 fully connected layer with dendritic branch gating), with inputs drawn i.i.d.
 from the stated normal distribution.
 
-Layout: X and its gradient are [T, N, B] with branches innermost and neurons
-ordered (batch, channel, spatial), N = batch * C * S.  Spikes and their
-gradient are [T, N].  Per-channel parameters are [C, B].
+Layout: X and its gradient are [T, N, P] with the P = B k compartments
+innermost (k per branch, a branch's compartments adjacent) and neurons ordered
+(batch, channel, spatial), N = batch * C * S.  Spikes and their gradient are
+[T, N].  Per-channel parameters are [C, B] (kappa, zeta, gating mask) and
+[C, P] (xi).
 """
 
 from __future__ import annotations
@@ -46,10 +48,16 @@ class Workload:
     mask_rho: float = 0.5
     stateful: bool = True
     detach_reset: bool = False
+    comps_per_branch: int = 1    # k = P / B
+    residual: bool = False       # residual dendrite (ResStateful / ResStateless)
 
     @property
     def N(self) -> int:
         return self.batch * self.C * self.S
+
+    @property
+    def P(self) -> int:
+        return self.B * self.comps_per_branch
 
     @property
     def nbs(self) -> int:
@@ -76,6 +84,17 @@ WORKLOADS = {
                              alpha=0.8, beta=0.9, ckpt_every=8),
     # Task-incremental fully connected layer with a per-task branch-gating mask.
     "dbg": Workload("dbg", T=4, batch=64, C=8192, S=1, B=32, tasks=10, mask_rho=0.5),
+    # The paper's common dendrite (P = 4 compartments on B = 2 branches) on the
+    # CIFAR-shaped conv activation.
+    "cifar_p4b2": Workload("cifar_p4b2", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2, x_std=0.5),
+    # ResStateless dendrite (Tiny-ImageNet-style deep network: 64x64 maps),
+    # identity activation, P = 4 on B = 2.
+    "tiny_imagenet_res": Workload("tiny_imagenet_res", T=4, batch=64, C=64, S=64 * 64, B=2, comps_per_branch=2,
+                                  psi="identity", stateful=False, residual=True),
+    # Stateless dendrite on a neuromorphic (CIFAR10-DVS-style) conv layer, T = 10,
+    # P = 10 compartments on B = 5 branches.
+    "dvs_p10b5": Workload("dvs_p10b5", T=10, batch=16, C=128, S=32 * 32, B=5, comps_per_branch=2,
+                          stateful=False),
 }
 
 
@@ -91,10 +110,10 @@ def params(wl: Workload, seed: int = 0, random_affine: bool = False):
     rng = np.random.default_rng([seed, 1])
     kappa = rng.uniform(0.0, 1.0, size=(wl.C, wl.B)).astype(np.float32)
     if random_affine:
-        xi = rng.normal(0.0, 0.5, size=(wl.C, wl.B)).astype(np.float32)
+        xi = rng.normal(0.0, 0.5, size=(wl.C, wl.P)).astype(np.float32)
         zeta = rng.uniform(0.5, 2.0, size=(wl.C, wl.B)).astype(np.float32)
     else:
-        xi = np.zeros((wl.C, wl.B), np.float32)
+        xi = np.zeros((wl.C, wl.P), np.float32)
         zeta = np.ones((wl.C, wl.B), np.float32)
     return dict(kappa=kappa, xi=xi, zeta=zeta)
 
@@ -106,7 +125,7 @@ def _torch_dtype(io: str):
 
 
 def activations(wl: Workload, device="cpu", seed: int = 0, batch: int | None = None):
-    """X [T, N, B] ~ N(x_mean, x_std) and the spike gradient gS [T, N] ~ N(0, 1),
+    """X [T, N, P] ~ N(x_mean, x_std) and the spike gradient gS [T, N] ~ N(0, 1),
     drawn in float32 by torch's generator on ``device`` and then stored in the
     workload's I/O dtype (bf16 by round-to-nearest-even)."""
     import torch
@@ -116,7 +135,7 @@ def activations(wl: Workload, device="cpu", seed: int = 0, batch: int | None = N
     g = torch.Generator(device=device)
     g.manual_seed(seed)
     dt = _torch_dtype(wl.io)
-    X = torch.empty((wl.T, N, wl.B), dtype=torch.float32, device=device)
+    X = torch.empty((wl.T, N, wl.P), dtype=torch.float32, device=device)
     X.normal_(wl.x_mean, wl.x_std, generator=g)
     gS = torch.empty((wl.T, N), dtype=torch.float32, device=device)
     gS.normal_(0.0, 1.0, generator=g)
