@@ -155,7 +155,7 @@ def main():
                               detach_reset=wl.detach_reset, ckpt_every=wl.ckpt_every, io=wl.io, psi=wl.psi,
                               sg=wl.sg, sg_scale=wl.sg_scale, beta=wl.beta, v_th=wl.v_th,
                               batch_groups=args.batch_groups, comps_per_branch=wl.comps_per_branch,
-                              residual=wl.residual)
+                              residual=wl.residual, layout=wl.layout)
     X, gS = workloads.activations(wl, device=dev, seed=0)
     p = workloads.params(wl, seed=0)
     kappa = torch.from_numpy(p["kappa"]).to(dev)
@@ -249,7 +249,7 @@ def main():
         "dtype": "f32" if wl.io == "f32" else "bf16 storage, f32 arithmetic",
         "data": "synthetic",
         "config": {"workload": wl.name, "T": wl.T, "batch": wl.batch, "C": wl.C, "S": wl.S, "B": wl.B,
-                   "P": wl.P, "N": wl.N, "io": wl.io, "psi": wl.psi, "surrogate": f"{wl.sg}({wl.sg_scale})",
+                   "P": wl.P, "layout": wl.layout, "N": wl.N, "io": wl.io, "psi": wl.psi, "surrogate": f"{wl.sg}({wl.sg_scale})",
                    "dendrite": ("res" if wl.residual else "") + ("stateful" if wl.stateful else "stateless"),
                    "alpha": wl.alpha, "beta": wl.beta, "v_th": wl.v_th, "ckpt_every": wl.K,
                    "tasks": n_tasks},

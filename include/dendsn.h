@@ -28,6 +28,11 @@
  * Layout (all row-major), with P = B * KC compartments per neuron:
  *   X, grad_x          [T, N, P]  compartments innermost, I/O dtype (fp32 or bf16); compartment
  *                                 i lies on branch i / KC (a branch's compartments are adjacent)
+ *                      or, with cfg->layout = DENDSN_LAYOUT_CHANNEL_MAJOR, [T, batch, C, P, S]:
+ *                                 the paper's layer layout (Methods, "Dendritic spiking neural
+ *                                 networks"), where the producing layer's C*P channels are cut
+ *                                 into groups of P consecutive feature maps, one group per
+ *                                 output channel (the same memory as [T, N, P] when S = 1)
  *   spikes, grad_spikes[T, N]     I/O dtype; spikes are exactly 0.0 or 1.0
  *   v_soma, grad_v_soma[T, N]     fp32; v_soma[t] = H[t], the potential before the reset
  *   kappa, zeta        [C, B]     fp32 per-channel branch parameters
@@ -78,6 +83,7 @@ typedef enum dendsn_status {
 typedef enum dendsn_io { DENDSN_IO_F32 = 0, DENDSN_IO_BF16 = 1 } dendsn_io;
 typedef enum dendsn_psi { DENDSN_PSI_IDENTITY = 0, DENDSN_PSI_MEXHAT = 1 } dendsn_psi;
 typedef enum dendsn_sg { DENDSN_SG_ATAN = 0, DENDSN_SG_SIGMOID = 1 } dendsn_sg;
+typedef enum dendsn_layout { DENDSN_LAYOUT_NPB = 0, DENDSN_LAYOUT_CHANNEL_MAJOR = 1 } dendsn_layout;
 
 typedef struct dendsn_cfg {
     int64_t T;                 /* time steps, >= 1                                         */
@@ -97,6 +103,7 @@ typedef struct dendsn_cfg {
     float v_th;                /* firing threshold (the paper uses 1)                       */
     int32_t batch_groups;      /* tuning: batch groups per launch, 0 = automatic           */
     int32_t residual;          /* 1: residual dendrite, Z += mean of the neuron's inputs   */
+    int32_t layout;            /* dendsn_layout of X and grad_x                            */
 } dendsn_cfg;
 
 /*

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdendsn.s
 IO = {"f32": 0, "bf16": 1}
 PSI = {"identity": 0, "mexhat": 1}
 SG = {"atan": 0, "sigmoid": 1}
+LAYOUT = {"npb": 0, "channel_major": 1}
 
 STATUS = {0: "DENDSN_OK", 1: "DENDSN_E_INVALID", 2: "DENDSN_E_UNSUPPORTED",
           3: "DENDSN_E_WORKSPACE", 4: "DENDSN_E_HIP"}
@@ -50,6 +51,7 @@ class dendsn_cfg(ctypes.Structure):
         ("v_th", ctypes.c_float),
         ("batch_groups", ctypes.c_int32),
         ("residual", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
     ]
 
 
@@ -75,6 +77,7 @@ class DendSNConfig:
     batch_groups: int = 0
     comps_per_branch: int = 1
     residual: bool = False
+    layout: str = "npb"          # X / grad_x: "npb" [T, N, P] or "channel_major" [T, batch, C, P, S]
 
     @property
     def N(self) -> int:
@@ -96,6 +99,7 @@ class DendSNConfig:
             ckpt_every=self.ckpt_every if self.ckpt_every > 0 else max(1, min(self.T, 2**31 - 1)),
             io=IO[self.io], psi=PSI[self.psi], sg=SG[self.sg], sg_scale=self.sg_scale,
             beta=self.beta, v_th=self.v_th, batch_groups=self.batch_groups, residual=int(self.residual),
+            layout=LAYOUT[self.layout],
         )
 
 
@@ -213,11 +217,22 @@ def _expect(t, name, shape, dtype, device, optional=False):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _x_shape(cfg, x):
+    """[T, N, P]; in the channel-major layout any contiguous shape that starts
+    with T and holds T N P elements in [T, batch, C, P, S] order (for example
+    the producing conv layer's [T, batch, C P, H, W])."""
+    if cfg.layout == "channel_major":
+        n = cfg.N * cfg.P
+        return tuple(x.shape) if (x.dim() >= 2 and x.shape[0] == cfg.T and x.numel() == cfg.T * n) \
+            else (cfg.T, cfg.batch, cfg.C, cfg.P, cfg.S)
+    return (cfg.T, cfg.N, cfg.P)
+
+
 def _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta=None):
     import torch
 
     dev = x.device
-    _expect(x, "x", (cfg.T, cfg.N, cfg.P), _io_dtype(cfg), dev)
+    _expect(x, "x", _x_shape(cfg, x), _io_dtype(cfg), dev)
     _expect(alpha, "alpha", (1,), torch.float32, dev, optional=not cfg.stateful)
     _expect(beta, "beta", (1,), torch.float32, dev, optional=True)
     _expect(kappa, "kappa", (cfg.C, cfg.B), torch.float32, dev)
@@ -244,7 +259,7 @@ def forward(cfg: DendSNConfig, x, alpha, kappa, xi=None, zeta=None, mask=None, *
 
 def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma=None,
              workspace=None, *, beta=None):
-    """Returns a dict with grad_x [T,N,P] io and grad_alpha [1], grad_beta [1],
+    """Returns a dict with grad_x (x's shape and layout) and grad_alpha [1], grad_beta [1],
     grad_kappa, grad_zeta [C,B] and grad_xi [C,P] (fp32)."""
     import torch
 
@@ -253,7 +268,7 @@ def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spik
     _expect(grad_spikes, "grad_spikes", (cfg.T, cfg.N), _io_dtype(cfg), dev)
     _expect(grad_v_soma, "grad_v_soma", (cfg.T, cfg.N), torch.float32, dev, optional=True)
     out = dict(
-        grad_x=torch.empty((cfg.T, cfg.N, cfg.P), dtype=_io_dtype(cfg), device=dev),
+        grad_x=torch.empty(x.shape, dtype=_io_dtype(cfg), device=dev),
         grad_alpha=torch.empty((1,), dtype=torch.float32, device=dev),
         grad_beta=torch.empty((1,), dtype=torch.float32, device=dev),
         grad_kappa=torch.empty((cfg.C, cfg.B), dtype=torch.float32, device=dev),

@@ -19,6 +19,10 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdendsn.so")
 
 SOURCES = [
+    "dendsn_fwd_f32_cm.hip",
+    "dendsn_fwd_bf16_cm.hip",
+    "dendsn_bwd_f32_cm.hip",
+    "dendsn_bwd_bf16_cm.hip",
     "dendsn_fwd_f32_kc.hip",
     "dendsn_fwd_bf16_kc.hip",
     "dendsn_bwd_f32_kc.hip",

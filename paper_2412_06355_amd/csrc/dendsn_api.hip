@@ -18,6 +18,10 @@ hipError_t launch_fwd_f32_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream
 hipError_t launch_fwd_bf16_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
 hipError_t launch_bwd_f32_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
 hipError_t launch_bwd_bf16_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_fwd_f32_cm(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
+hipError_t launch_fwd_bf16_cm(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_cm(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_cm(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
 
 // Fixed-order float64 sums of the per-block partials into the parameter
 // gradients.  Outputs o = c * W + ol with W = 2 B + P: ol < B is g_kappa of
@@ -126,6 +130,22 @@ bool choose_mapping(int B, int KC, int io, int* BL, int* L, int* fast) {
   return false;
 }
 
+// The channel-major layout (S > 1; with S = 1 it is the same memory as
+// [T, N, P]): the fewest lanes per neuron (a power of two dividing B) that leave
+// at most 4 compartments in a lane, if a compiled mapping has it.
+bool channel_major(const dendsn_cfg* c) { return c->layout == DENDSN_LAYOUT_CHANNEL_MAJOR && c->S > 1; }
+
+bool cm_mapping(int B, int KC, int* BL, int* L) {
+  int l = 1;
+  while ((B * KC) / l > 4 && B % (2 * l) == 0 && 2 * l <= 16) l *= 2;
+  const int bl = B / l;
+#define DENDSN_IN(BL_, L_, KC_) \
+  if (bl == BL_ && l == L_ && KC == KC_) { *BL = bl; *L = l; return true; }
+  DENDSN_CM(DENDSN_IN)
+#undef DENDSN_IN
+  return false;
+}
+
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 dendsn_status check_cfg(const dendsn_cfg* c) {
@@ -151,6 +171,8 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   if (!isfinite(c->v_th)) return fail(DENDSN_E_INVALID, "v_th must be finite");
   if (c->batch_groups < 0) return fail(DENDSN_E_INVALID, "batch_groups must be >= 0");
   if (c->residual != 0 && c->residual != 1) return fail(DENDSN_E_INVALID, "residual must be 0 or 1");
+  if (c->layout != DENDSN_LAYOUT_NPB && c->layout != DENDSN_LAYOUT_CHANNEL_MAJOR)
+    return fail(DENDSN_E_INVALID, "bad layout");
   // N and T * N * B must fit comfortably in int64 element counts.
   const int64_t lim = int64_t(1) << 46;
   if (c->batch > lim / c->C || c->batch * c->C > lim / c->S) return fail(DENDSN_E_INVALID, "N too large");
@@ -158,8 +180,12 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   const int64_t P = int64_t(c->B) * c->comps_per_branch;
   if (N > (lim / P) / c->T) return fail(DENDSN_E_INVALID, "T * N * P too large");
   int BL, L, fast;
-  if (!choose_mapping(c->B, c->comps_per_branch, c->io, &BL, &L, &fast))
+  if (channel_major(c)) {
+    if (!cm_mapping(c->B, c->comps_per_branch, &BL, &L))
+      return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build in the channel-major layout");
+  } else if (!choose_mapping(c->B, c->comps_per_branch, c->io, &BL, &L, &fast)) {
     return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build");
+  }
   return DENDSN_OK;
 }
 
@@ -168,8 +194,13 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
 Plan make_plan(const dendsn_cfg* c, bool bwd) {
   Plan p;
   memset(&p, 0, sizeof(p));
-  choose_mapping(c->B, c->comps_per_branch, c->io, &p.BL, &p.L, &p.fast);
   p.KC = c->comps_per_branch;
+  if (channel_major(c)) {
+    p.cm = 1; p.fast = 0;
+    cm_mapping(c->B, c->comps_per_branch, &p.BL, &p.L);
+  } else {
+    choose_mapping(c->B, c->comps_per_branch, c->io, &p.BL, &p.L, &p.fast);
+  }
   const int L = p.L;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
@@ -199,7 +230,7 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   p.G = int32_t(ceil_div(c->batch, p.bpg));
   const int64_t Ke = c->ckpt_every < c->T ? c->ckpt_every : c->T;
   p.nck = int32_t(ceil_div(c->T, c->ckpt_every) - 1);
-  p.KS = (p.fast && p.KC == 1 && p.BL <= 4 && Ke >= 8) ? 8 : 4;
+  p.KS = (p.fast && p.KC == 1 && !p.cm && p.BL <= 4 && Ke >= 8) ? 8 : 4;
   return p;
 }
 
@@ -236,6 +267,7 @@ void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* a
   s->M = c->C * c->S; s->N = c->batch * s->M;
   s->B = c->B;
   s->P = c->B * c->comps_per_branch;
+  s->xes = uint32_t((p.cm ? c->S : 1) * (c->io == DENDSN_IO_BF16 ? 2 : 4));
   s->K = int32_t(c->ckpt_every < c->T ? c->ckpt_every : c->T);
   s->nck = p.nck;
   s->beta = c->beta; s->vth = c->v_th;
@@ -307,8 +339,10 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   fa.ckpt = p.nck > 0 ? ckpt : nullptr;
   const int v = cfg->psi | (cfg->residual << 1);
   const bool bf = cfg->io == DENDSN_IO_BF16;
-  const hipError_t e = p.KC == 1 ? (bf ? launch_fwd_bf16(p, fa, v, stream) : launch_fwd_f32(p, fa, v, stream))
-                                 : (bf ? launch_fwd_bf16_kc(p, fa, v, stream) : launch_fwd_f32_kc(p, fa, v, stream));
+  const hipError_t e =
+      p.cm ? (bf ? launch_fwd_bf16_cm(p, fa, v, stream) : launch_fwd_f32_cm(p, fa, v, stream))
+      : p.KC == 1 ? (bf ? launch_fwd_bf16(p, fa, v, stream) : launch_fwd_f32(p, fa, v, stream))
+                  : (bf ? launch_fwd_bf16_kc(p, fa, v, stream) : launch_fwd_f32_kc(p, fa, v, stream));
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("forward launch: ") + hipGetErrorString(e));
   return DENDSN_OK;
 }
@@ -364,8 +398,10 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   ba.sg_scale = cfg->sg_scale;
   const int v = cfg->psi | (cfg->residual << 1);
   const bool bf = cfg->io == DENDSN_IO_BF16;
-  hipError_t e = p.KC == 1 ? (bf ? launch_bwd_bf16(p, ba, v, stream) : launch_bwd_f32(p, ba, v, stream))
-                           : (bf ? launch_bwd_bf16_kc(p, ba, v, stream) : launch_bwd_f32_kc(p, ba, v, stream));
+  hipError_t e =
+      p.cm ? (bf ? launch_bwd_bf16_cm(p, ba, v, stream) : launch_bwd_f32_cm(p, ba, v, stream))
+      : p.KC == 1 ? (bf ? launch_bwd_bf16(p, ba, v, stream) : launch_bwd_f32(p, ba, v, stream))
+                  : (bf ? launch_bwd_bf16_kc(p, ba, v, stream) : launch_bwd_f32_kc(p, ba, v, stream));
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("backward launch: ") + hipGetErrorString(e));
 
   FinArgs f;

@@ -27,11 +27,14 @@ typedef uint16_t bf16_t;  // bf16 storage
 
 // Kernel variant V: bit 0 = Mexican-hat activation (else identity), bit 1 =
 // residual dendrite (Z also receives the mean synaptic input of the neuron),
-// bits 2-3 = log2 of the compartments per branch KC (1, 2 or 4).  A lane holds
-// BL branches, i.e. E = BL * KC consecutive compartments of its neuron.
+// bits 2-3 = log2 of the compartments per branch KC (1, 2 or 4), bit 4 =
+// channel-major X / grad_x ([T, batch, C, P, S]: a neuron's compartments S
+// elements apart).  A lane holds BL branches, i.e. E = BL * KC compartments of
+// its neuron.
 template <int V> constexpr bool kMH = (V & 1) != 0;
 template <int V> constexpr bool kRes = (V & 2) != 0;
 template <int V> constexpr int kKC = 1 << ((V >> 2) & 3);
+template <int V> constexpr bool kCM = (V & 16) != 0;
 
 // -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.721347520444481703680f;
@@ -215,6 +218,31 @@ __device__ __forceinline__ void store_vec_nt(bf16_t* __restrict__ p, const float
 
 __device__ __forceinline__ float load_one(const float* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__builtin_nontemporal_load(p)); }
+__device__ __forceinline__ void store_one_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ void store_one_nt(bf16_t* p, float v) { __builtin_nontemporal_store(to_bf16(v), p); }
+
+// A lane's E compartments of X / grad_x: adjacent (a vector access) or, in the
+// channel-major layout, es bytes apart (one access each; the lanes of a wave
+// hold adjacent positions, so each access is contiguous across the wave).
+template <int E, bool CM, typename IO>
+__device__ __forceinline__ void load_x(const IO* p, uint32_t es, float (&v)[E]) {
+  if constexpr (CM) {
+#pragma unroll
+    for (int i = 0; i < E; ++i) v[i] = load_one(at(p, uint32_t(i) * es));
+  } else {
+    load_vec<E>(p, v);
+  }
+}
+
+template <int E, bool CM, typename IO>
+__device__ __forceinline__ void store_gx(IO* p, uint32_t es, const float (&v)[E]) {
+  if constexpr (CM) {
+#pragma unroll
+    for (int i = 0; i < E; ++i) store_one_nt(at(p, uint32_t(i) * es), v[i]);
+  } else {
+    store_vec_nt<E>(p, v);
+  }
+}
 __device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
 __device__ __forceinline__ void store_spike(bf16_t* p, bool s) { *p = s ? bf16_t(0x3f80) : bf16_t(0); }
 
@@ -406,10 +434,13 @@ struct LaneOff {
   uint32_t v;   // fp32 per-neuron rows (v_soma, grad_v_soma, checkpointed H)
 };
 
-template <typename IO, int E>
+template <typename IO, int E, bool CM>
 __device__ __forceinline__ LaneOff lane_offsets(const ScanArgs& a, const Pos& pos) {
   LaneOff o;
-  o.x = uint32_t((pos.m * a.P + pos.sub * E) * int64_t(sizeof(IO)));
+  // channel-major: compartment i of position s = m - c S of channel c sits at
+  // (c P + i) S + s; this lane's first compartment is i = sub E
+  o.x = CM ? uint32_t((pos.m + pos.c * (a.P - 1) * a.S + int64_t(pos.sub) * E * a.S) * int64_t(sizeof(IO)))
+           : uint32_t((pos.m * a.P + pos.sub * E) * int64_t(sizeof(IO)));
   o.c = uint32_t((pos.m * a.P + pos.sub * E) * 4);
   o.s = uint32_t(pos.m * int64_t(sizeof(IO)));
   o.v = uint32_t(pos.m * 4);
@@ -438,13 +469,13 @@ struct RowCursor {  // wave-uniform position of the next chunk to load
   int k, t;         // neuron index in the lane's list, first row of the chunk
 };
 
-template <typename IO, int BL, int D>
+template <bool CM, typename IO, int BL, int D>
 __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, D>& cur, uint32_t ox, int T,
                                            int Tp, int64_t rowX, int64_t item_stride, float (&buf)[D][BL]) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = min(cur.t + k, T - 1);
-    load_vec<BL>(at(cur.base + int64_t(t) * rowX, ox), buf[k]);
+    load_x<BL, CM>(at(cur.base + int64_t(t) * rowX, ox), a.xes, buf[k]);
   }
   cur.t += D;
   if (cur.t >= Tp) {
@@ -531,7 +562,7 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   Branches<BL, kKC<V>> br;
   load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br);
   const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-  const LaneOff lo = lane_offsets<IO, E>(a, pos);
+  const LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
   const bool lead = pos.sub == 0;
   const int T = int(a.T);
   const int Tp = (T + D - 1) / D * D;
@@ -549,11 +580,11 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   fwd_item_start<IO, E>(fa, bt0 * a.M, st);
 
   float bufA[D][E], bufB[D][E];
-  if (nchunks > 0) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
+  if (nchunks > 0) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
   for (int c = 0; c < nchunks; c += 2) {
-    if (c + 1 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufB);
+    if (c + 1 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufB);
     compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
-    if (c + 2 < nchunks) load_chunk(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
+    if (c + 2 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
     if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
   }
 }
@@ -606,14 +637,14 @@ __device__ __forceinline__ void load_chunk_gv(const ScanArgs& a, const LaneOff& 
   }
 }
 
-template <typename IO, int E, int CS>
+template <typename IO, int E, int CS, bool CM>
 __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
                                               const IO* gsbase, const float* gvbase, int c0, ChunkIn<E, CS>& in) {
   const int64_t rowX = a.N * a.P;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
     const int64_t t = c0 + k;
-    load_vec<E>(at(xbase + t * rowX, lo.x), in.x[k]);
+    load_x<E, CM>(at(xbase + t * rowX, lo.x), a.xes, in.x[k]);
     in.gs[k] = load_one(at(gsbase + t * a.N, lo.s));
   }
   load_chunk_gv<E, CS>(a, lo, gvbase, c0, in);
@@ -748,7 +779,7 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
         acc.z[j] = fmaf(-g * gzu, br.rz[j], acc.z[j]);
       }
     }
-    store_vec_nt<E>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), gxo);
+    store_gx<E, kCM<V>>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), a.xes, gxo);
     bl.dh_next = dh;
   }
 }
@@ -772,7 +803,7 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
   const int64_t rowX = a.N * a.P;
   for (int t = t_from; t < t_to; ++t) {
     float xv[E];
-    load_vec<E>(at(xbase + int64_t(t) * rowX, lo.x), xv);
+    load_x<E, kCM<V>>(at(xbase + int64_t(t) * rowX, lo.x), a.xes, xv);
     const float z = dendrite_step<BL, L, V>(vd, xv, br, alpha);
     soma_step(h, s, z, a.beta, a.vth);
   }
@@ -786,7 +817,7 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
                                                    BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
   constexpr int E = BL * kKC<V>;
   ChunkIn<E, CS> in;
-  load_chunk_in<IO, E, CS>(ba.s, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+  load_chunk_in<IO, E, CS, kCM<V>>(ba.s, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
   float v[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) v[j] = ss.v[j];
@@ -836,7 +867,7 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
     for (int ch = nfull - 1; ch >= 0; --ch) {
       const int c0 = t0 + rem + ch * KS;
       ChunkIn<E, KS> in;
-      load_chunk_in<IO, E, KS>(a, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
+      load_chunk_in<IO, E, KS, kCM<V>>(a, lo, bl.xbase, bl.gsbase, bl.gvbase, c0, in);
       float v[E];
 #pragma unroll
       for (int j = 0; j < E; ++j) v[j] = ss.v[j];
@@ -878,7 +909,7 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
   ChunkIn<E, KS> cur;
-  if (nk > 0) load_chunk_in<IO, E, KS>(a, lo, x + n0 * a.P, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
+  if (nk > 0) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + n0 * a.P, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
   float zero[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) zero[j] = 0.0f;
@@ -895,7 +926,7 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
     recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
     ChunkIn<E, KS> nxt;
     const int64_t n1 = n0 + step;
-    if (i + 1 < nk) load_chunk_in<IO, E, KS>(a, lo, x + n1 * a.P, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
+    if (i + 1 < nk) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + n1 * a.P, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
     reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
     cur = nxt;
     n0 = n1;
@@ -1033,7 +1064,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     Branches<BL, kKC<V>> br;
     load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br);
     const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-    const LaneOff lo = lane_offsets<IO, E>(a, pos);
+    const LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
     int64_t bt0;
     const int nk = items_of(a, pos, &bt0);
     const int T = int(a.T);

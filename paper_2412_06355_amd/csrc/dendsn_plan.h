@@ -21,6 +21,7 @@ struct Plan {
   int32_t BL;     // branches held by one lane
   int32_t L;      // lanes per neuron (power of two, <= 16); B = BL * L
   int32_t KC;     // compartments per branch (1, 2 or 4); a lane holds BL * KC of them
+  int32_t cm;     // 1: channel-major X / grad_x (a neuron's compartments S apart)
   int32_t fast;   // 1: a vector-width mapping with every stash capacity compiled
   int32_t mode;   // TileMode
   int32_t ways;   // batch ways inside a block (waves that share positions)
@@ -43,7 +44,8 @@ struct ScanArgs {
   const uint8_t* mask;  // NULL: all branches kept
   const float* beta_p;  // learnable somatic decay on the device, or NULL: beta
   int64_t T, N, C, S, M, batch;  // M = C * S positions per sample
-  int32_t B, P, K, nck;          // P = B * KC compartments: the innermost extent of X
+  int32_t B, P, K, nck;          // P = B * KC compartments per neuron
+  uint32_t xes;                  // bytes between a neuron's compartments in X / grad_x
   float beta, vth;
   float rP;             // 1 / P (residual dendrite)
   int32_t mode, ways, pb, tpc, cpt, bpg;
@@ -108,5 +110,12 @@ constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread p
                                X(2, 1, 4) X(2, 2, 4) X(2, 4, 4) X(2, 8, 4) X(2, 16, 4)
 #define DENDSN_KC_GENERIC(X) X(1, 1, 2) X(2, 1, 2) X(3, 1, 2) X(5, 1, 2) X(6, 1, 2) X(7, 1, 2) \
                              X(1, 1, 4) X(2, 1, 4) X(3, 1, 4)
+
+// Compiled (BL, L, KC) for the channel-major layout (stash capacity 4): the
+// fewest lanes per neuron that leave at most 4 compartments in a lane with
+// whole branches in each.
+#define DENDSN_CM(X) X(1, 1, 1) X(2, 1, 1) X(3, 1, 1) X(4, 1, 1) X(5, 1, 1) X(7, 1, 1) X(3, 2, 1) \
+                     X(4, 2, 1) X(4, 4, 1) X(1, 1, 2) X(2, 1, 2) X(3, 1, 2) X(2, 2, 2) X(2, 4, 2) \
+                     X(1, 1, 4) X(1, 2, 4) X(1, 4, 4)
 
 }  // namespace dendsn

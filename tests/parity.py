@@ -108,14 +108,27 @@ def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True,
 # ---------------------------------------------------------------------------
 # GPU side
 # ---------------------------------------------------------------------------
+def to_channel_major(cfg, a: np.ndarray) -> np.ndarray:
+    """[T, N, P] (N ordered batch, C, S) -> [T, batch, C, P, S]."""
+    T = a.shape[0]
+    return np.ascontiguousarray(a.reshape(T, cfg.batch, cfg.C, cfg.S, cfg.P).transpose(0, 1, 2, 4, 3))
+
+
+def from_channel_major(cfg, a: np.ndarray) -> np.ndarray:
+    T = a.shape[0]
+    return np.ascontiguousarray(a.reshape(T, cfg.batch, cfg.C, cfg.P, cfg.S).transpose(0, 1, 2, 4, 3)
+                                .reshape(T, cfg.N, cfg.P))
+
+
 def to_device(case: Case, device):
     import torch
 
     io = torch.bfloat16 if case.cfg.io == "bf16" else torch.float32
+    X = to_channel_major(case.cfg, case.X) if case.cfg.layout == "channel_major" else case.X
     t = lambda a, dt=torch.float32: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(
         device=device, dtype=dt)
     return dict(
-        x=t(case.X, io), gS=t(case.gS, io), gV=t(case.gV),
+        x=t(X, io), gS=t(case.gS, io), gV=t(case.gV),
         alpha=torch.tensor([case.alpha], dtype=torch.float32, device=device),
         beta=None if case.beta_dev is None else torch.tensor([case.beta_dev], dtype=torch.float32,
                                                              device=device),
@@ -138,7 +151,10 @@ def run_gpu(case: Case, device, dev=None, want_v_soma=True):
                         d["gS"], d["gV"], beta=d["beta"])
     torch.cuda.synchronize(device)
     f = lambda t: None if t is None else t.float().cpu().numpy().astype(np.float64)
-    return dict(S=f(spikes), H=f(v_soma), gX=f(g["grad_x"]), g_alpha=float(g["grad_alpha"].item()),
+    gX = f(g["grad_x"])
+    if case.cfg.layout == "channel_major":
+        gX = from_channel_major(case.cfg, gX)
+    return dict(S=f(spikes), H=f(v_soma), gX=gX, g_alpha=float(g["grad_alpha"].item()),
                 g_beta=float(g["grad_beta"].item()), g_kappa=f(g["grad_kappa"]), g_xi=f(g["grad_xi"]), g_zeta=f(g["grad_zeta"]),
                 raw=dict(spikes=spikes, v_soma=v_soma, grads=g))
 

@@ -29,7 +29,8 @@ def header_functions():
 
 def base_cfg(**kw):
     c = dict(T=4, batch=2, C=256, S=1, B=4, comps_per_branch=1, stateful=1, detach_reset=0,
-             ckpt_every=4, io=0, psi=1, sg=1, sg_scale=4.0, beta=0.5, v_th=1.0, batch_groups=0, residual=0)
+             ckpt_every=4, io=0, psi=1, sg=1, sg_scale=4.0, beta=0.5, v_th=1.0, batch_groups=0, residual=0,
+             layout=0)
     c.update(kw)
     return dendsn_cfg(**c)
 
@@ -105,6 +106,9 @@ def test_workspace_bytes_positive_and_grows_with_groups(lib):
     (dict(beta=float("inf")), E_INVALID), (dict(v_th=float("nan")), E_INVALID),
     (dict(batch_groups=-1), E_INVALID), (dict(batch=1 << 40, C=1 << 10), E_INVALID),
     (dict(residual=2), E_INVALID), (dict(residual=-1), E_INVALID),
+    (dict(layout=2), E_INVALID), (dict(layout=-1), E_INVALID),
+    (dict(layout=1, S=4, B=64), E_UNSUPPORTED), (dict(layout=1, S=4, B=16, comps_per_branch=2), E_UNSUPPORTED),
+    (dict(layout=1, S=4, B=3, comps_per_branch=4), E_UNSUPPORTED), (dict(layout=1, S=4, B=9), E_UNSUPPORTED),
 ])
 def test_bad_cfg_rejected_everywhere(lib, kw, code):
     cfg = base_cfg(**kw)
@@ -187,3 +191,15 @@ def test_supported_compartment_layouts(lib, io, B, k):
     out = ctypes.c_size_t(0)
     assert lib.dendsn_bwd_workspace_bytes(ctypes.byref(cfg), ctypes.byref(out)) == OK
     assert out.value > 0
+
+
+def test_channel_major_layout_limits(lib):
+    """Channel-major X with S > 1 supports the compiled lane splits (up to 16
+    branches / 16 compartments); with S = 1 it is the [T, N, P] memory and every
+    mapping applies."""
+    out = ctypes.c_size_t(0)
+    for B, k in [(1, 1), (5, 1), (6, 1), (7, 1), (8, 1), (16, 1), (4, 1), (4, 2), (8, 2),
+                 (3, 2), (2, 4), (4, 4)]:
+        assert lib.dendsn_ckpt_bytes(ctypes.byref(base_cfg(layout=1, S=9, B=B, comps_per_branch=k)),
+                                     ctypes.byref(out)) == OK
+    assert lib.dendsn_ckpt_bytes(ctypes.byref(base_cfg(layout=1, S=1, B=64)), ctypes.byref(out)) == OK

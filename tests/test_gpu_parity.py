@@ -152,6 +152,56 @@ def test_replicated_compartments_match_one_compartment(gpu_device):
     assert np.all((g1["S"] == gk["S"]) | near)
 
 
+# --- the paper's channel-major layer layout [T, batch, C, P, S] ---
+CM_SHAPES = [
+    # T, batch, C, S, B, k, io, K
+    (4, 2, 3, 300, 4, 1, "f32", 4),      # spatial tiles (S >= 256), P = 4
+    (5, 2, 7, 33, 8, 1, "f32", 2),       # whole channels per tile, P = 8
+    (4, 3, 4, 257, 2, 2, "f32", 4),      # the paper's P = 4 on B = 2
+    (6, 2, 5, 20, 1, 4, "bf16", 3),
+    (4, 2, 3, 513, 4, 1, "bf16", 4),
+    (7, 2, 6, 5, 3, 2, "f32", 7),        # P = 6
+    (3, 2, 4, 64, 5, 1, "bf16", 3),
+    (9, 1, 2, 300, 2, 4, "f32", 4),      # P = 8, checkpoints
+    (4, 2, 3, 260, 16, 1, "f32", 4),     # 4 lanes per neuron
+    (5, 2, 4, 70, 6, 1, "bf16", 5),      # 2 lanes of 3 branches
+    (4, 2, 3, 300, 8, 2, "f32", 2),      # P = 16 over 4 lanes
+    (6, 2, 5, 31, 4, 4, "bf16", 4),      # P = 16, k = 4, 4 lanes
+    (4, 2, 2, 400, 7, 1, "f32", 4),      # odd branch count, one lane
+]
+
+
+@pytest.mark.parametrize("shape", CM_SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}k{}{}K{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "id-atan-stateless-res-plif"])
+def test_channel_major_layout(gpu_device, shape, variant):
+    T, batch, C, S, B, k, io, K = shape
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, comps_per_branch=k, io=io, ckpt_every=K, layout="channel_major",
+            psi="identity" if "-id-" in f"-{variant}-" else "mexhat", sg="sigmoid" if "sig" in variant else "atan",
+            stateful="stateless" not in variant, residual="res" in variant, beta=0.7)
+    seed = zlib.crc32(repr((shape, variant, "cm")).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6, mask_rho=0.5 if "mask" in variant else None,
+                     name=f"cm/{shape}/{variant}", beta_dev=0.8 if "plif" in variant else None)
+    compare(case, run_gpu(case, gpu_device))
+
+
+@pytest.mark.parametrize("B,k,io", [(4, 1, "f32"), (8, 1, "f32"), (2, 2, "f32"), (4, 1, "bf16"), (16, 1, "f32"),
+                                    (8, 2, "bf16")])
+def test_channel_major_equals_compartments_innermost(gpu_device, B, k, io):
+    """Same neurons, same per-lane arithmetic order: the two layouts give
+    bit-identical spikes, potentials and input gradients (after the permutation)."""
+    import torch
+
+    base = cfg(T=5, batch=2, C=6, S=300, B=B, comps_per_branch=k, io=io, ckpt_every=3)
+    case = make_case(base, seed=33, mask_rho=0.6, name=f"cm-vs-npb/B{B}k{k}{io}")
+    a = run_gpu(case, gpu_device)
+    case.cfg = base.with_(layout="channel_major")
+    b = run_gpu(case, gpu_device)
+    assert torch.equal(a["raw"]["spikes"], b["raw"]["spikes"])
+    assert torch.equal(a["raw"]["v_soma"], b["raw"]["v_soma"])
+    assert np.array_equal(a["gX"], b["gX"])
+    compare(case, b)
+
+
 # --- residual dendrite (ResStateful / ResStateless) and the PLIF soma ---
 @pytest.mark.parametrize("stateful", [True, False])
 @pytest.mark.parametrize("plif", [False, True])

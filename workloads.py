@@ -50,6 +50,7 @@ class Workload:
     detach_reset: bool = False
     comps_per_branch: int = 1    # k = P / B
     residual: bool = False       # residual dendrite (ResStateful / ResStateless)
+    layout: str = "npb"          # X / grad_x layout: [T, N, P] or "channel_major" [T, batch, C, P, S]
 
     @property
     def N(self) -> int:
@@ -87,6 +88,11 @@ WORKLOADS = {
     # The paper's common dendrite (P = 4 compartments on B = 2 branches) on the
     # CIFAR-shaped conv activation.
     "cifar_p4b2": Workload("cifar_p4b2", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2, x_std=0.5),
+    # The same layer consuming the producing conv layer's output as it is laid
+    # out, [T, batch, C P, H, W] (groups of P consecutive feature maps).
+    "cifar_p4b2_cm": Workload("cifar_p4b2_cm", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2, x_std=0.5,
+                              layout="channel_major"),
+    "cifar_cm": Workload("cifar_cm", T=4, batch=128, C=128, S=32 * 32, B=8, x_std=0.5, layout="channel_major"),
     # ResStateless dendrite (Tiny-ImageNet-style deep network: 64x64 maps),
     # identity activation, P = 4 on B = 2.
     "tiny_imagenet_res": Workload("tiny_imagenet_res", T=4, batch=64, C=64, S=64 * 64, B=2, comps_per_branch=2,
@@ -125,7 +131,8 @@ def _torch_dtype(io: str):
 
 
 def activations(wl: Workload, device="cpu", seed: int = 0, batch: int | None = None):
-    """X [T, N, P] ~ N(x_mean, x_std) and the spike gradient gS [T, N] ~ N(0, 1),
+    """X [T, N, P] ~ N(x_mean, x_std) (i.i.d., so the same draw serves the
+    channel-major layout) and the spike gradient gS [T, N] ~ N(0, 1),
     drawn in float32 by torch's generator on ``device`` and then stored in the
     workload's I/O dtype (bf16 by round-to-nearest-even)."""
     import torch
