@@ -221,28 +221,176 @@ __device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__bu
 __device__ __forceinline__ void store_one_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 __device__ __forceinline__ void store_one_nt(bf16_t* p, float v) { __builtin_nontemporal_store(to_bf16(v), p); }
 
-// A lane's E compartments of X / grad_x: adjacent (a vector access) or, in the
-// channel-major layout, es bytes apart (one access each; the lanes of a wave
-// hold adjacent positions, so each access is contiguous across the wave).
-template <int E, bool CM, typename IO>
-__device__ __forceinline__ void load_x(const IO* p, uint32_t es, float (&v)[E]) {
-  if constexpr (CM) {
+// ---------------------------------------------------------------------------
+// Streamed rows through buffer resources: the row base is wave-uniform (scalar
+// registers, the resource), the lane's part a 32-bit offset, and a further
+// uniform part rides in the instruction's scalar offset, so no per-lane 64-bit
+// address arithmetic is spent on the backward's X, grad_spikes and grad_x rows.  Accesses
+// are non-temporal (each byte is touched once per pass).
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kAuxNT = 2;  // cache policy: non-temporal (streaming)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  // raw buffer, byte range 4 GiB - 1 (every lane offset is a uint32 below it)
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
+}
+
+template <int BL>
+__device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL], const float*) {
+  if constexpr (BL % 4 == 0) {
 #pragma unroll
-    for (int i = 0; i < E; ++i) v[i] = load_one(at(p, uint32_t(i) * es));
+    for (int i = 0; i < BL / 4; ++i) {
+      const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16u * i, 0, kAuxNT);
+      v[4 * i] = __uint_as_float(q.x); v[4 * i + 1] = __uint_as_float(q.y);
+      v[4 * i + 2] = __uint_as_float(q.z); v[4 * i + 3] = __uint_as_float(q.w);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const u32x2_t q = __builtin_amdgcn_raw_buffer_load_b64(r, off + 8u * i, 0, kAuxNT);
+      v[2 * i] = __uint_as_float(q.x); v[2 * i + 1] = __uint_as_float(q.y);
+    }
   } else {
-    load_vec<E>(p, v);
+#pragma unroll
+    for (int i = 0; i < BL; ++i) v[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off + 4u * i, 0, kAuxNT));
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL], const bf16_t*) {
+  if constexpr (BL % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 8; ++i) {
+      const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16u * i, 0, kAuxNT);
+      v[8 * i + 0] = bf16_lo(q.x); v[8 * i + 1] = bf16_hi(q.x);
+      v[8 * i + 2] = bf16_lo(q.y); v[8 * i + 3] = bf16_hi(q.y);
+      v[8 * i + 4] = bf16_lo(q.z); v[8 * i + 5] = bf16_hi(q.z);
+      v[8 * i + 6] = bf16_lo(q.w); v[8 * i + 7] = bf16_hi(q.w);
+    }
+  } else if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const u32x2_t q = __builtin_amdgcn_raw_buffer_load_b64(r, off + 8u * i, 0, kAuxNT);
+      v[4 * i + 0] = bf16_lo(q.x); v[4 * i + 1] = bf16_hi(q.x);
+      v[4 * i + 2] = bf16_lo(q.y); v[4 * i + 3] = bf16_hi(q.y);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const uint32_t q = __builtin_amdgcn_raw_buffer_load_b32(r, off + 4u * i, 0, kAuxNT);
+      v[2 * i] = bf16_lo(q); v[2 * i + 1] = bf16_hi(q);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i)
+      v[i] = bf16_lo(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off + 2u * i, 0, kAuxNT)));
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void bstore_vec(rsrc_t r, uint32_t off, const float (&v)[BL], float*) {
+  if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const u32x4_t q = {__float_as_uint(v[4 * i]), __float_as_uint(v[4 * i + 1]), __float_as_uint(v[4 * i + 2]),
+                         __float_as_uint(v[4 * i + 3])};
+      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, kAuxNT);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i) {
+      const u32x2_t q = {__float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1])};
+      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, kAuxNT);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), r, off + 4u * i, 0, kAuxNT);
+  }
+}
+
+template <int BL>
+__device__ __forceinline__ void bstore_vec(rsrc_t r, uint32_t off, const float (&v)[BL], bf16_t*) {
+  if constexpr (BL % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 8; ++i) {
+      const u32x4_t q = {pack_bf16x2(v[8 * i + 0], v[8 * i + 1]), pack_bf16x2(v[8 * i + 2], v[8 * i + 3]),
+                         pack_bf16x2(v[8 * i + 4], v[8 * i + 5]), pack_bf16x2(v[8 * i + 6], v[8 * i + 7])};
+      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, kAuxNT);
+    }
+  } else if constexpr (BL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 4; ++i) {
+      const u32x2_t q = {pack_bf16x2(v[4 * i + 0], v[4 * i + 1]), pack_bf16x2(v[4 * i + 2], v[4 * i + 3])};
+      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, kAuxNT);
+    }
+  } else if constexpr (BL % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < BL / 2; ++i)
+      __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(v[2 * i], v[2 * i + 1]), r, off + 4u * i, 0, kAuxNT);
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v[i]), r, off + 2u * i, 0, kAuxNT);
+  }
+}
+
+__device__ __forceinline__ float bload_one(rsrc_t r, uint32_t off, uint32_t soff, const float*) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, soff, kAuxNT));
+}
+__device__ __forceinline__ float bload_one(rsrc_t r, uint32_t off, uint32_t soff, const bf16_t*) {
+  return bf16_lo(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, soff, kAuxNT)));
+}
+__device__ __forceinline__ void bstore_one(rsrc_t r, uint32_t off, uint32_t soff, float v, float*) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, soff, kAuxNT);
+}
+__device__ __forceinline__ void bstore_one(rsrc_t r, uint32_t off, uint32_t soff, float v, bf16_t*) {
+  __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v), r, off, soff, kAuxNT);
+}
+
+// A lane's E compartments of X / grad_x in the row starting at `row`: adjacent
+// (a vector access at the lane offset) or, in the channel-major layout, es
+// bytes apart (one access each, the uniform i * es in the scalar offset; the
+// lanes of a wave hold adjacent positions, so each access is contiguous across
+// the wave).
+// BUF: through a buffer resource (measured faster in the backward, where
+// VALU issue is the co-limiter), else a global access at base + offset
+// (measured faster in the forward).
+template <int E, bool CM, bool BUF, typename IO>
+__device__ __forceinline__ void load_x(const IO* row, uint32_t off, uint32_t es, float (&v)[E]) {
+  if constexpr (!BUF) {
+    if constexpr (CM) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] = load_one(at(row, off + uint32_t(i) * es));
+    } else {
+      load_vec<E>(at(row, off), v);
+    }
+  } else {
+    const rsrc_t r = make_rsrc(row);
+    if constexpr (CM) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] = bload_one(r, off, uint32_t(i) * es, row);
+    } else {
+      bload_vec<E>(r, off, v, row);
+    }
   }
 }
 
 template <int E, bool CM, typename IO>
-__device__ __forceinline__ void store_gx(IO* p, uint32_t es, const float (&v)[E]) {
+__device__ __forceinline__ void store_gx(IO* row, uint32_t off, uint32_t es, const float (&v)[E]) {
+  const rsrc_t r = make_rsrc(row);
   if constexpr (CM) {
 #pragma unroll
-    for (int i = 0; i < E; ++i) store_one_nt(at(p, uint32_t(i) * es), v[i]);
+    for (int i = 0; i < E; ++i) bstore_one(r, off, uint32_t(i) * es, v[i], row);
   } else {
-    store_vec_nt<E>(p, v);
+    bstore_vec<E>(r, off, v, row);
   }
 }
+
+template <typename IO>
+__device__ __forceinline__ float load_row_one(const IO* row, uint32_t off) {
+  return bload_one(make_rsrc(row), off, 0, row);
+}
+
 __device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
 __device__ __forceinline__ void store_spike(bf16_t* p, bool s) { *p = s ? bf16_t(0x3f80) : bf16_t(0); }
 
@@ -293,6 +441,7 @@ struct Branches {
   float k[BL];        // kappa * m  (0 for a gated-off branch)
   float xi[BL * KC];  // per compartment
   float rz[BL];       // 1 / zeta
+  float krz[BL];      // kappa* / zeta
   bool on[BL];        // mask bit
   float rp;           // 1 / P, the residual term's weight of each compartment
 };
@@ -306,6 +455,7 @@ __device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int 
     br.on[j] = on;
     br.k[j] = on ? a.kappa[base + j] : 0.0f;
     br.rz[j] = a.zeta ? 1.0f / a.zeta[base + j] : 1.0f;
+    br.krz[j] = br.k[j] * br.rz[j];
   }
   const int64_t base_i = c * a.P + int64_t(sub) * (BL * KC);
 #pragma unroll
@@ -356,7 +506,7 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL * kKC<V>], const f
       const float q = tt * tt;
       const float e = __builtin_amdgcn_exp2f(q * kNegHalfLog2e);
       if (efac) efac[j] = e;
-      y = (1.0f - q) * e;
+      y = fmaf(-q, e, e);  // (1 - q) e
     } else {
       y = KC == 1 ? fabsf(tt) : tt;
     }
@@ -475,7 +625,7 @@ __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, 
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = min(cur.t + k, T - 1);
-    load_x<BL, CM>(at(cur.base + int64_t(t) * rowX, ox), a.xes, buf[k]);
+    load_x<BL, CM, false>(cur.base + int64_t(t) * rowX, ox, a.xes, buf[k]);
   }
   cur.t += D;
   if (cur.t >= Tp) {
@@ -644,8 +794,8 @@ __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& 
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
     const int64_t t = c0 + k;
-    load_x<E, CM>(at(xbase + t * rowX, lo.x), a.xes, in.x[k]);
-    in.gs[k] = load_one(at(gsbase + t * a.N, lo.s));
+    load_x<E, CM, true>(xbase + t * rowX, lo.x, a.xes, in.x[k]);
+    in.gs[k] = load_row_one(gsbase + t * a.N, lo.s);
   }
   load_chunk_gv<E, CS>(a, lo, gvbase, c0, in);
 }
@@ -731,17 +881,17 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
     for (int j = 0; j < BL; ++j) {
       if constexpr (KC == 1) {
         const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
-        float y, dps;  // psi(u) and psi'(u) sgn(Vd - xi)
+        const float dhk = dh * br.krz[j];
+        float y, r;  // psi(u), and r = kappa* dH psi'(u) sgn(Vd - xi) / zeta
         if constexpr (kMH<V>) {
           const float q = tt * tt;
           const float e = st.e[kMH<V> ? k : 0][j];
-          y = (1.0f - q) * e;
-          dps = tt * (q - 3.0f) * e;
+          y = fmaf(-q, e, e);                          // (1 - q) e, rounded as in the forward
+          r = dhk * (tt * fmaf(-3.0f, e, q * e));      // psi'(u) sgn = tt (q - 3) e
         } else {
           y = fabsf(tt);
-          dps = tt > 0.0f ? 1.0f : (tt < 0.0f ? -1.0f : 0.0f);
+          r = tt > 0.0f ? dhk : (tt < 0.0f ? -dhk : 0.0f);
         }
-        const float r = (br.k[j] * dh) * dps * br.rz[j];
         bl.lam[j] = fmaf(alpha, bl.lam[j], r);
         gxo[j] = kRes<V> ? fmaf(dh, br.rp, bl.lam[j]) : bl.lam[j];
         acc.k[j] = fmaf(dh, y, acc.k[j]);
@@ -753,18 +903,18 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
         // du/dVd_i = rz d_i / ||d|| (0 at ||d|| = 0), du/dzeta = -u rz.
         const float nrm = __builtin_amdgcn_sqrtf(branch_sumsq<KC>(&st.v[k + 1][j * KC], &br.xi[j * KC]));
         const float u = nrm * br.rz[j];
-        const float g = br.k[j] * dh;
+        const float dhk = dh * br.krz[j];          // kappa* dH / zeta
         float y, w, gzu;  // psi(u), the factor of d_i in dL/dVd_i, and psi'(u) u
         if constexpr (kMH<V>) {
           const float q = u * u;
           const float e = st.e[kMH<V> ? k : 0][j];
-          y = (1.0f - q) * e;
-          const float qe = (q - 3.0f) * e;          // psi'(u) / u
-          w = g * qe * (br.rz[j] * br.rz[j]);        // g psi'(u) rz / ||d||
+          y = fmaf(-q, e, e);                        // (1 - q) e, rounded as in the forward
+          const float qe = fmaf(-3.0f, e, q * e);    // psi'(u) / u = (q - 3) e
+          w = dhk * (qe * br.rz[j]);                 // kappa* dH psi'(u) rz / ||d||
           gzu = qe * q;
         } else {
           y = u;
-          w = nrm > 0.0f ? g * br.rz[j] * __builtin_amdgcn_rcpf(nrm) : 0.0f;
+          w = nrm > 0.0f ? dhk * __builtin_amdgcn_rcpf(nrm) : 0.0f;
           gzu = u;
         }
 #pragma unroll
@@ -776,10 +926,10 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
           acc.a = fmaf(bl.lam[i], st.v[k][i], acc.a);
         }
         acc.k[j] = fmaf(dh, y, acc.k[j]);
-        acc.z[j] = fmaf(-g * gzu, br.rz[j], acc.z[j]);
+        acc.z[j] = fmaf(-dhk, gzu, acc.z[j]);     // -kappa* dH psi'(u) u / zeta
       }
     }
-    store_gx<E, kCM<V>>(at(bl.gxbase + int64_t(c0 + k) * rowX, lo.x), a.xes, gxo);
+    store_gx<E, kCM<V>>(bl.gxbase + int64_t(c0 + k) * rowX, lo.x, a.xes, gxo);
     bl.dh_next = dh;
   }
 }
@@ -803,7 +953,7 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
   const int64_t rowX = a.N * a.P;
   for (int t = t_from; t < t_to; ++t) {
     float xv[E];
-    load_x<E, kCM<V>>(at(xbase + int64_t(t) * rowX, lo.x), a.xes, xv);
+    load_x<E, kCM<V>, true>(xbase + int64_t(t) * rowX, lo.x, a.xes, xv);
     const float z = dendrite_step<BL, L, V>(vd, xv, br, alpha);
     soma_step(h, s, z, a.beta, a.vth);
   }
