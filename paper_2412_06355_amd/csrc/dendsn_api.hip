@@ -231,6 +231,13 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   const int64_t Ke = c->ckpt_every < c->T ? c->ckpt_every : c->T;
   p.nck = int32_t(ceil_div(c->T, c->ckpt_every) - 1);
   p.KS = (p.fast && p.KC == 1 && !p.cm && p.BL <= 4 && Ke >= 8) ? 8 : 4;
+  // Occupancy cap (measured on MI355X): the backward over conv-shaped tiles whose
+  // lanes move 16 bytes per row runs 3-4 % faster with at most two blocks per CU
+  // (fewer concurrent streams contending for DRAM pages); with 8-byte rows (bf16,
+  // four branches) or the fully connected tiling the cap costs 15-17 %.  Unused
+  // dynamic LDS reserves the room.
+  const int esz = c->io == DENDSN_IO_BF16 ? 2 : 4;
+  p.lds = (bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16) ? int32_t(163840 / 3 + 256) : 0;
   return p;
 }
 

@@ -5,12 +5,12 @@
 namespace dendsn {
 
 template <int BL, int L, int KS>
-static hipError_t launch_bwd_v(const dim3& grid, const BwdArgs& ba, int v, hipStream_t stream) {
+static hipError_t launch_bwd_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
   switch (v) {
-    case 0: dendsn_bwd_kernel<float, BL, L, 0, KS><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<float, BL, L, 1, KS><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<float, BL, L, 2, KS><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<float, BL, L, 3, KS><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
+    case 0: dendsn_bwd_kernel<float, BL, L, 0, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 1: dendsn_bwd_kernel<float, BL, L, 1, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 2: dendsn_bwd_kernel<float, BL, L, 2, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 3: dendsn_bwd_kernel<float, BL, L, 3, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -20,14 +20,14 @@ hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int v, hipStream_t 
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
 #define DENDSN_FAST_CASE(BL_, L_)                                                   \
   if (pl.BL == BL_ && pl.L == L_ && pl.fast) {                                      \
-    if (pl.KS == 4) return launch_bwd_v<BL_, L_, 4>(grid, ba, v, stream);           \
+    if (pl.KS == 4) return launch_bwd_v<BL_, L_, 4>(grid, ba, v, size_t(pl.lds), stream);           \
     if constexpr (BL_ <= 4)                                                         \
-      if (pl.KS == 8) return launch_bwd_v<BL_, L_, 8>(grid, ba, v, stream);         \
+      if (pl.KS == 8) return launch_bwd_v<BL_, L_, 8>(grid, ba, v, size_t(pl.lds), stream);         \
     return hipErrorInvalidValue;                                                    \
   }
 #define DENDSN_GENERIC_CASE(BL_, L_)                                                \
   if (pl.BL == BL_ && pl.L == L_ && !pl.fast && pl.KS == DENDSN_GENERIC_KS)         \
-    return launch_bwd_v<BL_, L_, DENDSN_GENERIC_KS>(grid, ba, v, stream);
+    return launch_bwd_v<BL_, L_, DENDSN_GENERIC_KS>(grid, ba, v, size_t(pl.lds), stream);
   DENDSN_FAST_F32(DENDSN_FAST_CASE)
   DENDSN_GENERIC(DENDSN_GENERIC_CASE)
 #undef DENDSN_FAST_CASE

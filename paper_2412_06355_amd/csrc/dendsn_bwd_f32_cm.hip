@@ -7,13 +7,13 @@
 namespace dendsn {
 
 template <int BL, int L, int KC>
-static hipError_t launch_bwd_cm_v(const dim3& grid, const BwdArgs& ba, int v, hipStream_t stream) {
+static hipError_t launch_bwd_cm_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = 16 | ((KC == 1 ? 0 : (KC == 2 ? 1 : 2)) << 2);
   switch (v & 3) {
-    case 0: dendsn_bwd_kernel<float, BL, L, VK | 0, 4><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<float, BL, L, VK | 1, 4><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<float, BL, L, VK | 2, 4><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<float, BL, L, VK | 3, 4><<<grid, dim3(kThreads), 0, stream>>>(ba); break;
+    case 0: dendsn_bwd_kernel<float, BL, L, VK | 0, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 1: dendsn_bwd_kernel<float, BL, L, VK | 1, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 2: dendsn_bwd_kernel<float, BL, L, VK | 2, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 3: dendsn_bwd_kernel<float, BL, L, VK | 3, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
   }
   return hipGetLastError();
 }
@@ -22,7 +22,7 @@ hipError_t launch_bwd_f32_cm(const Plan& pl, const BwdArgs& ba, int v, hipStream
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
   if (!pl.cm || pl.KS != 4) return hipErrorInvalidValue;
 #define DENDSN_CASE(BL_, L_, KC_) \
-  if (pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_bwd_cm_v<BL_, L_, KC_>(grid, ba, v, stream);
+  if (pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_bwd_cm_v<BL_, L_, KC_>(grid, ba, v, size_t(pl.lds), stream);
   DENDSN_CM(DENDSN_CASE)
 #undef DENDSN_CASE
   return hipErrorInvalidValue;

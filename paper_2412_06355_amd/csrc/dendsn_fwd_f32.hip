@@ -5,12 +5,12 @@
 namespace dendsn {
 
 template <int BL, int L>
-static hipError_t launch_fwd_v(const dim3& grid, const FwdArgs& fa, int v, hipStream_t stream) {
+static hipError_t launch_fwd_v(const dim3& grid, const FwdArgs& fa, int v, size_t lds, hipStream_t stream) {
   switch (v) {
-    case 0: dendsn_fwd_kernel<float, BL, L, 0><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 1: dendsn_fwd_kernel<float, BL, L, 1><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 2: dendsn_fwd_kernel<float, BL, L, 2><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 3: dendsn_fwd_kernel<float, BL, L, 3><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 0: dendsn_fwd_kernel<float, BL, L, 0><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 1: dendsn_fwd_kernel<float, BL, L, 1><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 2: dendsn_fwd_kernel<float, BL, L, 2><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 3: dendsn_fwd_kernel<float, BL, L, 3><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -19,7 +19,7 @@ static hipError_t launch_fwd_v(const dim3& grid, const FwdArgs& fa, int v, hipSt
 hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
 #define DENDSN_CASE(BL_, L_) \
-  if (pl.BL == BL_ && pl.L == L_) return launch_fwd_v<BL_, L_>(grid, fa, v, stream);
+  if (pl.BL == BL_ && pl.L == L_) return launch_fwd_v<BL_, L_>(grid, fa, v, size_t(pl.lds), stream);
   DENDSN_FAST_F32(DENDSN_CASE)
   DENDSN_GENERIC(DENDSN_CASE)
 #undef DENDSN_CASE

@@ -7,13 +7,13 @@
 namespace dendsn {
 
 template <int BL, int L, int KC>
-static hipError_t launch_fwd_cm_v(const dim3& grid, const FwdArgs& fa, int v, hipStream_t stream) {
+static hipError_t launch_fwd_cm_v(const dim3& grid, const FwdArgs& fa, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = 16 | ((KC == 1 ? 0 : (KC == 2 ? 1 : 2)) << 2);
   switch (v & 3) {
-    case 0: dendsn_fwd_kernel<float, BL, L, VK | 0><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 1: dendsn_fwd_kernel<float, BL, L, VK | 1><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 2: dendsn_fwd_kernel<float, BL, L, VK | 2><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 3: dendsn_fwd_kernel<float, BL, L, VK | 3><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 0: dendsn_fwd_kernel<float, BL, L, VK | 0><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 1: dendsn_fwd_kernel<float, BL, L, VK | 1><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 2: dendsn_fwd_kernel<float, BL, L, VK | 2><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 3: dendsn_fwd_kernel<float, BL, L, VK | 3><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
   }
   return hipGetLastError();
 }
@@ -22,7 +22,7 @@ hipError_t launch_fwd_f32_cm(const Plan& pl, const FwdArgs& fa, int v, hipStream
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
   if (!pl.cm) return hipErrorInvalidValue;
 #define DENDSN_CASE(BL_, L_, KC_) \
-  if (pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_cm_v<BL_, L_, KC_>(grid, fa, v, stream);
+  if (pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_cm_v<BL_, L_, KC_>(grid, fa, v, size_t(pl.lds), stream);
   DENDSN_CM(DENDSN_CASE)
 #undef DENDSN_CASE
   return hipErrorInvalidValue;

@@ -6,13 +6,13 @@
 namespace dendsn {
 
 template <int BL, int L, int KC>
-static hipError_t launch_fwd_kc_v(const dim3& grid, const FwdArgs& fa, int v, hipStream_t stream) {
+static hipError_t launch_fwd_kc_v(const dim3& grid, const FwdArgs& fa, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = (KC == 2 ? 1 : 2) << 2;
   switch (v & 3) {
-    case 0: dendsn_fwd_kernel<float, BL, L, VK | 0><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 1: dendsn_fwd_kernel<float, BL, L, VK | 1><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 2: dendsn_fwd_kernel<float, BL, L, VK | 2><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
-    case 3: dendsn_fwd_kernel<float, BL, L, VK | 3><<<grid, dim3(kThreads), 0, stream>>>(fa); break;
+    case 0: dendsn_fwd_kernel<float, BL, L, VK | 0><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 1: dendsn_fwd_kernel<float, BL, L, VK | 1><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 2: dendsn_fwd_kernel<float, BL, L, VK | 2><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    case 3: dendsn_fwd_kernel<float, BL, L, VK | 3><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
   }
   return hipGetLastError();
 }
@@ -20,9 +20,9 @@ static hipError_t launch_fwd_kc_v(const dim3& grid, const FwdArgs& fa, int v, hi
 hipError_t launch_fwd_f32_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
 #define DENDSN_FAST_CASE(BL_, L_, KC_) \
-  if (pl.fast && pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_kc_v<BL_, L_, KC_>(grid, fa, v, stream);
+  if (pl.fast && pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_kc_v<BL_, L_, KC_>(grid, fa, v, size_t(pl.lds), stream);
 #define DENDSN_GENERIC_CASE(BL_, L_, KC_) \
-  if (!pl.fast && pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_kc_v<BL_, L_, KC_>(grid, fa, v, stream);
+  if (!pl.fast && pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_kc_v<BL_, L_, KC_>(grid, fa, v, size_t(pl.lds), stream);
   DENDSN_KC_FAST_F32(DENDSN_FAST_CASE)
   DENDSN_KC_GENERIC(DENDSN_GENERIC_CASE)
 #undef DENDSN_FAST_CASE

@@ -33,6 +33,7 @@ struct Plan {
   int32_t bpg;    // batch items per group
   int32_t KS;     // backward stash capacity in steps (compile-time in the kernel)
   int32_t nck;    // interior checkpoints, ceil(T / K) - 1
+  int32_t lds;    // dynamic LDS bytes per block, reserved only to cap blocks per CU
 };
 
 struct ScanArgs {
