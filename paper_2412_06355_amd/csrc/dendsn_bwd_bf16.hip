@@ -28,7 +28,7 @@ hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int v, hipStream_t
 #define DENDSN_GENERIC_CASE(BL_, L_)                                                \
   if (pl.BL == BL_ && pl.L == L_ && !pl.fast && pl.KS == DENDSN_GENERIC_KS)         \
     return launch_bwd_v<BL_, L_, DENDSN_GENERIC_KS>(grid, ba, v, size_t(pl.lds), stream);
-  DENDSN_FAST_BF16(DENDSN_FAST_CASE)
+  DENDSN_FAST_BF16_BWD(DENDSN_FAST_CASE)
   DENDSN_GENERIC(DENDSN_GENERIC_CASE)
 #undef DENDSN_FAST_CASE
 #undef DENDSN_GENERIC_CASE

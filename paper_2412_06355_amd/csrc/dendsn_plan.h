@@ -93,11 +93,17 @@ struct FinArgs {
 constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread per output
 
 // Compiled (BL, L) mappings with one compartment per branch.  "Fast" mappings
-// move 8 or 16 bytes per lane; "generic" ones cover other branch counts.
+// move 8 or 16 bytes per lane; "generic" ones cover other branch counts.  For
+// powers of two the branch sum is the same balanced tree whatever the split
+// of the neuron over lanes (pairwise in a lane, then the DPP butterfly), so
+// the forward and the backward may split a neuron differently and still agree
+// bit for bit.
 // Backward stash capacities: 4 steps for every mapping, and 8 steps too when a
 // lane holds at most 4 branches.
 #define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
 #define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
+// The bf16 backward also holds 4 branches per lane (8 bytes) up to 64 branches.
+#define DENDSN_FAST_BF16_BWD(X) DENDSN_FAST_BF16(X) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
 #define DENDSN_GENERIC(X) X(1, 1) X(2, 1) X(3, 1) X(5, 1) X(6, 1) X(7, 1) X(5, 2) X(6, 2) X(7, 2)
 #define DENDSN_GENERIC_KS 4
 

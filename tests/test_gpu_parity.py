@@ -63,6 +63,9 @@ SHAPES = [
     (16, 3, 3, 2, 8, "f32", 16),
     (13, 2, 6, 1, 8, "bf16", 13),
     (10, 2, 4, 100, 2, "f32", 10),
+    (6, 2, 20, 1, 16, "bf16", 3),     # bf16 backward splits a neuron differently from the forward
+    (4, 2, 9, 40, 32, "bf16", 4),
+    (5, 2, 3, 1, 64, "bf16", 2),
 ]
 
 
@@ -293,6 +296,26 @@ def test_checkpoint_interval_is_bit_invariant(gpu_device):
         assert torch.equal(o["spikes"], ref["spikes"])
         assert torch.equal(o["v_soma"], ref["v_soma"])
         assert torch.equal(_bits(o["grads"]["grad_x"]), _bits(ref["grads"]["grad_x"]))
+
+
+@pytest.mark.parametrize("B,io", [(8, "bf16"), (16, "bf16"), (64, "bf16"), (16, "f32")])
+def test_recompute_from_checkpoints_is_bit_exact(gpu_device, B, io):
+    """The backward recomputes the forward from state checkpoints; it must reproduce
+    the forward's states bit for bit even where it splits a neuron over lanes
+    differently (bf16), so every checkpoint interval gives the same bits."""
+    import torch
+
+    base = cfg(T=24, batch=2, C=40, S=1, B=B, io=io, beta=0.9, ckpt_every=6)
+    case = make_case(base, seed=18, x_mean=0.1, alpha=0.8, mask_rho=0.7, name=f"ckpt-bits/B{B}{io}")
+    d = to_device(case, gpu_device)
+    outs = []
+    for K in (6, 24, 1):
+        case.cfg = base.with_(ckpt_every=K)
+        outs.append(run_gpu(case, gpu_device, dev=d)["raw"])
+    for o in outs[1:]:
+        assert torch.equal(o["spikes"], outs[0]["spikes"])
+        assert torch.equal(_bits(o["grads"]["grad_x"]), _bits(outs[0]["grads"]["grad_x"]))
+    compare(case, run_gpu(case, gpu_device, dev=d))
 
 
 def test_run_to_run_determinism(gpu_device):
