@@ -255,7 +255,7 @@ REDUCED = {
     "cifar_p4b2": dict(T=4, batch=2, C=128, S=1024, B=2, comps_per_branch=2, x_std=0.5),
     "tiny_imagenet_res": dict(T=4, batch=1, C=64, S=4096, B=2, comps_per_branch=2, psi="identity",
                               stateful=False, residual=True),
-    "dvs_p10b5": dict(T=10, batch=1, C=128, S=1024, B=5, comps_per_branch=2, stateful=False),
+    "dvs_p10b5": dict(T=10, batch=1, C=128, S=1024, B=5, comps_per_branch=2, stateful=False, ckpt_every=4),
 }
 
 

@@ -100,9 +100,10 @@ WORKLOADS = {
     "tiny_imagenet_res": Workload("tiny_imagenet_res", T=4, batch=64, C=64, S=64 * 64, B=2, comps_per_branch=2,
                                   psi="identity", stateful=False, residual=True),
     # Stateless dendrite on a neuromorphic (CIFAR10-DVS-style) conv layer, T = 10,
-    # P = 10 compartments on B = 5 branches.
+    # P = 10 compartments on B = 5 branches (one lane holds a whole neuron).
+    # A state checkpoint every 4 steps keeps the backward's re-advance short.
     "dvs_p10b5": Workload("dvs_p10b5", T=10, batch=16, C=128, S=32 * 32, B=5, comps_per_branch=2,
-                          stateful=False),
+                          stateful=False, ckpt_every=4),
 }
 
 
