@@ -203,3 +203,27 @@ def test_channel_major_layout_limits(lib):
         assert lib.dendsn_ckpt_bytes(ctypes.byref(base_cfg(layout=1, S=9, B=B, comps_per_branch=k)),
                                      ctypes.byref(out)) == OK
     assert lib.dendsn_ckpt_bytes(ctypes.byref(base_cfg(layout=1, S=1, B=64)), ctypes.byref(out)) == OK
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    """No fallback: with the shared library absent every call raises."""
+    from paper_2412_06355_amd import binding
+
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "libdendsn.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        binding.dendsn_ckpt_bytes(dendsn.DendSNConfig(T=4, batch=2, C=4, S=1, B=4))
+
+
+def test_product_code_never_touches_the_oracle():
+    """The oracle is test infrastructure: the package and the C sources do not
+    import, link or name it."""
+    pkg = os.path.join(ROOT, "paper_2412_06355_amd")
+    for base, _, files in os.walk(pkg):
+        if "_build" in base:
+            continue
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(base, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "dendsn_oracle" not in text, f
