@@ -1,11 +1,13 @@
 // DendSN layer scan kernels for gfx950 (CDNA4, wave64).
 //
-// One kernel per direction.  A neuron's B branches are held by L adjacent lanes
-// of one wavefront, BL = B / L branches per lane, so one time step of X for a
-// wave is one contiguous, fully coalesced stretch of [T, N, B] memory.  The
-// dendritic states stay in registers across the time loop; the only cross-lane
-// traffic is the branch-to-soma sum Z, reduced with DPP inside the L-lane group,
-// and every lane of the group then runs the soma redundantly (no broadcast).
+// One kernel per direction.  A neuron's B branches (P = B KC compartments) are
+// held by L adjacent lanes of one wavefront, BL = B / L whole branches per lane,
+// so one time step of X for a wave is one contiguous, fully coalesced stretch of
+// [T, N, P] memory (or, in the channel-major layout, KC BL accesses that are each
+// contiguous across the wave).  The dendritic states stay in registers across
+// the time loop; the only cross-lane traffic is the branch-to-soma sum Z,
+// reduced with DPP inside the L-lane group, and every lane of the group then
+// runs the soma redundantly (no broadcast).
 //
 // A block owns a tile of positions of one sample (see TileMode) and loops over a
 // group of batch items, so per-channel parameters are loaded once per lane and
@@ -170,56 +172,8 @@ __device__ __forceinline__ const P* at(const P* base, uint32_t off) {
   return reinterpret_cast<const P*>(reinterpret_cast<const char*>(base) + off);
 }
 
-// grad_x is written once and never read back by the kernels: non-temporal stores.
-template <int BL>
-__device__ __forceinline__ void store_vec_nt(float* __restrict__ p, const float (&v)[BL]) {
-  if constexpr (BL % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 4; ++i) {
-      const f32x4_t q = {v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
-      __builtin_nontemporal_store(q, reinterpret_cast<f32x4_t*>(p) + i);
-    }
-  } else if constexpr (BL % 2 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 2; ++i) {
-      const f32x2_t q = {v[2 * i], v[2 * i + 1]};
-      __builtin_nontemporal_store(q, reinterpret_cast<f32x2_t*>(p) + i);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < BL; ++i) __builtin_nontemporal_store(v[i], p + i);
-  }
-}
-
-template <int BL>
-__device__ __forceinline__ void store_vec_nt(bf16_t* __restrict__ p, const float (&v)[BL]) {
-  if constexpr (BL % 8 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 8; ++i) {
-      const u32x4_t q = {pack_bf16x2(v[8 * i + 0], v[8 * i + 1]), pack_bf16x2(v[8 * i + 2], v[8 * i + 3]),
-                         pack_bf16x2(v[8 * i + 4], v[8 * i + 5]), pack_bf16x2(v[8 * i + 6], v[8 * i + 7])};
-      __builtin_nontemporal_store(q, reinterpret_cast<u32x4_t*>(p) + i);
-    }
-  } else if constexpr (BL % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 4; ++i) {
-      const u32x2_t q = {pack_bf16x2(v[4 * i + 0], v[4 * i + 1]), pack_bf16x2(v[4 * i + 2], v[4 * i + 3])};
-      __builtin_nontemporal_store(q, reinterpret_cast<u32x2_t*>(p) + i);
-    }
-  } else if constexpr (BL % 2 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 2; ++i)
-      __builtin_nontemporal_store(pack_bf16x2(v[2 * i], v[2 * i + 1]), reinterpret_cast<uint32_t*>(p) + i);
-  } else {
-#pragma unroll
-    for (int i = 0; i < BL; ++i) __builtin_nontemporal_store(to_bf16(v[i]), p + i);
-  }
-}
-
 __device__ __forceinline__ float load_one(const float* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__builtin_nontemporal_load(p)); }
-__device__ __forceinline__ void store_one_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
-__device__ __forceinline__ void store_one_nt(bf16_t* p, float v) { __builtin_nontemporal_store(to_bf16(v), p); }
 
 // ---------------------------------------------------------------------------
 // Streamed rows through buffer resources: the row base is wave-uniform (scalar
