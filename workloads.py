@@ -90,6 +90,8 @@ WORKLOADS = {
     # The paper's common dendrite (P = 4 compartments on B = 2 branches) on the
     # CIFAR-shaped conv activation.
     "cifar_p4b2": Workload("cifar_p4b2", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2, x_std=0.5),
+    "cifar_p4b2_bf16": Workload("cifar_p4b2_bf16", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2,
+                                x_std=0.5, io="bf16"),
     # The same layer consuming the producing conv layer's output as it is laid
     # out, [T, batch, C P, H, W] (groups of P consecutive feature maps).
     "cifar_p4b2_cm": Workload("cifar_p4b2_cm", T=4, batch=128, C=128, S=32 * 32, B=2, comps_per_branch=2, x_std=0.5,
