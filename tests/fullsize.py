@@ -1,0 +1,74 @@
+"""Per-batch-item oracle check for the full-size parity tests (runs in worker
+processes).  Neurons of different batch items are independent in both
+directions, so item b of a layer is checked on its own: spikes (forced-spike
+protocol), v_soma and grad_x element by element, and the item's parameter-
+gradient contributions are returned to be summed over all items in float64."""
+
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from tests.parity import BAND, RTOL_BF16, RTOL_F32
+
+
+def _open(spec):
+    path, shape = spec
+    return np.memmap(path, dtype=np.float32, mode="r", shape=tuple(shape))
+
+
+def check_item(job: dict) -> dict:
+    b, M, T = job["item"], job["M"], job["T"]
+    sl = slice(b * M, (b + 1) * M)
+    X = np.asarray(_open(job["X"])[:, sl, :], dtype=np.float64)
+    gS = np.asarray(_open(job["gS"])[:, sl], dtype=np.float64)
+    S_g = np.asarray(_open(job["S"])[:, sl], dtype=np.float64)
+    H_g = np.asarray(_open(job["H"])[:, sl], dtype=np.float64)
+    gX_g = np.asarray(_open(job["gX"])[:, sl, :], dtype=np.float64)
+    p = job["params"]
+    kw = dict(alpha=p["alpha"], beta=p["beta"], v_th=p["v_th"], kappa=p["kappa"], xi=p["xi"], zeta=p["zeta"],
+              mask=p["mask"], C=p["C"], S=p["S"], psi_kind=p["psi"], stateful=p["stateful"],
+              residual=p["residual"], comps_per_branch=p["k"])
+    # forced-spike protocol: impose the kernel's decision only where the oracle's
+    # potential is within BAND of the threshold
+    force = -np.ones((T, M), dtype=np.int64)
+    exempt = 0
+    for _ in range(T + 1):
+        rec = oracle.forward(X, force=force if exempt else None, **kw)
+        diff = rec["S"] != S_g
+        if not diff.any():
+            break
+        cols = np.nonzero(diff.any(axis=0))[0]
+        t_first = diff[:, cols].argmax(axis=0)
+        dist = np.abs(rec["H"][t_first, cols] - p["v_th"])
+        if np.any(dist > BAND):
+            i = int(np.argmax(dist > BAND))
+            return dict(item=b, error=f"item {b}: spike mismatch outside the band at t={t_first[i]}, "
+                                      f"neuron {cols[i]}: |H - v_th| = {dist[i]:.3e}")
+        force[t_first, cols] = S_g[t_first, cols].astype(np.int64)
+        exempt += len(cols)
+    else:
+        return dict(item=b, error=f"item {b}: forced-spike protocol did not converge")
+    g = oracle.backward(rec, gS, sg_kind=p["sg"], sg_scale=p["sg_scale"], detach_reset=p["detach"])
+    out = dict(item=b, error=None, exempt=exempt)
+    # elementwise comparisons of this item's outputs (scale: |o| + rms over the item)
+    for name, got, ref, rtol in (("v_soma", H_g, rec["H"], RTOL_F32 * job["growth"]),
+                                 ("grad_x", gX_g, g["gX"], job["rtol_io"] * job["growth"])):
+        scale = np.abs(ref) + np.sqrt(np.mean(ref * ref))
+        ratio = float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-300)))
+        out["max_" + name] = ratio
+        if ratio > rtol:
+            out["error"] = f"item {b}: {name} error/scale {ratio:.3e} > {rtol:.3g}"
+            return out
+        den = np.linalg.norm(ref)
+        nrel = float(np.linalg.norm(got - ref) / den) if den > 0 else 0.0
+        if nrel > (RTOL_F32 if name == "v_soma" else job["rtol_io"]):
+            out["error"] = f"item {b}: {name} norm-wise error {nrel:.3e}"
+            return out
+    for k in ("kappa", "xi", "zeta"):
+        out["g_" + k] = g["g_" + k]
+        out["abs_" + k] = g["abs_" + k]
+    for k in ("alpha", "beta"):
+        out["g_" + k] = g["g_" + k]
+        out["abs_" + k] = g["abs_" + k]
+    return out

@@ -1,0 +1,85 @@
+"""Parity at the benchmark's full layer sizes, in the launch configuration
+bench.py times (same cfg, automatic batch groups): every batch item's spikes,
+v_soma and grad_x are checked against the float64 oracle, run item by item in a
+pool of host processes, and the parameter gradients against the oracle's sums
+over all items.  Inputs are the benchmark's own seeded draws."""
+
+import multiprocessing as mp
+import os
+
+import numpy as np
+import pytest
+
+import paper_2412_06355_amd as dendsn
+import workloads
+from tests.fullsize import check_item
+from tests.parity import RTOL_BF16, RTOL_F32, announce, horizon_growth
+
+pytestmark = pytest.mark.gpu
+
+
+def _dump(t, path):
+    a = t.float().cpu().numpy()
+    mm = np.memmap(path, dtype=np.float32, mode="w+", shape=a.shape)
+    mm[...] = a
+    mm.flush()
+    return (str(path), list(a.shape))
+
+
+@pytest.mark.parametrize("name", ["cifar", "imagenet_stem", "long_horizon", "dbg"])
+def test_full_size_against_oracle(gpu_device, name, tmp_path):
+    import torch
+
+    wl = workloads.WORKLOADS[name]
+    announce(f"full-size parity {name}: T={wl.T} batch={wl.batch} C={wl.C} S={wl.S} B={wl.B} {wl.io}")
+    cfg = dendsn.DendSNConfig(T=wl.T, batch=wl.batch, C=wl.C, S=wl.S, B=wl.B, stateful=wl.stateful,
+                              detach_reset=wl.detach_reset, ckpt_every=wl.ckpt_every, io=wl.io, psi=wl.psi,
+                              sg=wl.sg, sg_scale=wl.sg_scale, beta=wl.beta, v_th=wl.v_th,
+                              comps_per_branch=wl.comps_per_branch, residual=wl.residual, layout=wl.layout)
+    X, gS = workloads.activations(wl, device=gpu_device, seed=0)
+    p = workloads.params(wl, seed=0)
+    kappa = torch.from_numpy(p["kappa"]).to(gpu_device)
+    alpha = torch.tensor([wl.alpha], dtype=torch.float32, device=gpu_device)
+    mask_np = workloads.branch_mask(wl.C, wl.B, 1, wl.mask_rho) if wl.tasks else None
+    mask = torch.from_numpy(mask_np).to(gpu_device) if mask_np is not None else None
+    spikes, v_soma, ckpt = dendsn.forward(cfg, X, alpha, kappa, None, None, mask, want_v_soma=True)
+    g = dendsn.backward(cfg, X, alpha, kappa, None, None, mask, ckpt, gS)
+    torch.cuda.synchronize(gpu_device)
+
+    files = dict(X=_dump(X, tmp_path / "X.f32"), gS=_dump(gS, tmp_path / "gS.f32"),
+                 S=_dump(spikes, tmp_path / "S.f32"), H=_dump(v_soma, tmp_path / "H.f32"),
+                 gX=_dump(g["grad_x"], tmp_path / "gX.f32"))
+    grads = {k: g[k].cpu().numpy().astype(np.float64) for k in ("grad_kappa", "grad_xi", "grad_zeta")}
+    g_alpha, g_beta = float(g["grad_alpha"].item()), float(g["grad_beta"].item())
+    del X, gS, spikes, v_soma, ckpt, g
+    torch.cuda.empty_cache()
+
+    params = dict(alpha=wl.alpha if wl.stateful else 0.0, beta=wl.beta, v_th=wl.v_th, kappa=p["kappa"],
+                  xi=None, zeta=None, mask=mask_np, C=wl.C, S=wl.S, psi=wl.psi, stateful=wl.stateful,
+                  residual=wl.residual, k=wl.comps_per_branch, sg=wl.sg, sg_scale=wl.sg_scale,
+                  detach=wl.detach_reset)
+    growth = horizon_growth(cfg, wl.alpha, wl.beta)
+    rtol_io = RTOL_BF16 if wl.io == "bf16" else RTOL_F32
+    jobs = [dict(item=b, M=wl.C * wl.S, T=wl.T, params=params, growth=growth, rtol_io=rtol_io, **files)
+            for b in range(wl.batch)]
+    workers = int(min(16, len(os.sched_getaffinity(0)), wl.batch))
+    with mp.get_context("spawn").Pool(workers) as pool:
+        res = pool.map(check_item, jobs, chunksize=1)
+    errors = [r["error"] for r in res if r["error"]]
+    assert not errors, errors[:5]
+    exempt = sum(r["exempt"] for r in res)
+    announce(f"full-size parity {name}: {wl.batch} items, {exempt} near-threshold exemptions")
+
+    def summed(key):
+        return sum(r[key] for r in res)
+
+    for k in ("kappa", "xi", "zeta"):
+        o, a = summed("g_" + k), summed("abs_" + k)
+        got = grads["grad_" + k]
+        scale = a + np.sqrt(np.mean(a * a))
+        err = np.abs(got - o)
+        assert np.all(err <= RTOL_F32 * growth * scale), (k, float(np.max(err / scale)))
+        assert np.linalg.norm(got - o) <= RTOL_F32 * np.linalg.norm(o), k
+    if wl.stateful:
+        assert abs(g_alpha - summed("g_alpha")) <= RTOL_F32 * growth * summed("abs_alpha")
+    assert abs(g_beta - summed("g_beta")) <= RTOL_F32 * growth * summed("abs_beta")
