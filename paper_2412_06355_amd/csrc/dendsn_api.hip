@@ -206,8 +206,18 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
     choose_mapping(c->B, c->comps_per_branch, c->io, bwd, &p.BL, &p.L, &p.fast);
   }
   const int L = p.L;
+  const int esz = c->io == DENDSN_IO_BF16 ? 2 : 4;
+  p.nw = 1;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
+    // The four-step backward over whole tiles of 16-byte lane rows takes two
+    // positions per lane and item (a wave then reads 2 x 64 / L adjacent
+    // positions per row): measured 3-9 % faster on the fp32 conv layers, and
+    // 2 % slower with the 8-byte rows of bf16.
+    if (bwd && c->T == 4 && !p.cm && p.BL * p.KC * esz == 16 && c->S % (2 * p.pb) == 0) {
+      p.nw = 2;
+      p.pb *= 2;
+    }
     p.tpc = int32_t(ceil_div(c->S, p.pb)); p.cpt = 1;
     p.ntiles = c->C * p.tpc;
   } else if (c->S == 1) {
@@ -237,11 +247,13 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   p.KS = (p.fast && p.KC == 1 && !p.cm && p.BL <= 4 && Ke >= 8) ? 8 : 4;
   // Occupancy cap (measured on MI355X): the backward over conv-shaped tiles whose
   // lanes move 16 bytes per row runs 3-4 % faster with at most two blocks per CU
-  // (fewer concurrent streams contending for DRAM pages); with 8-byte rows (bf16,
-  // four branches) or the fully connected tiling the cap costs 15-17 %.  Unused
-  // dynamic LDS reserves the room.
-  const int esz = c->io == DENDSN_IO_BF16 ? 2 : 4;
-  p.lds = (bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16) ? int32_t(163840 / 3 + 256) : 0;
+  // (fewer concurrent streams contending for DRAM pages), and with two positions
+  // per lane still 4 % faster when a neuron spans two or more lanes, but 1-2 %
+  // slower with one lane per neuron; with 8-byte rows (bf16, four branches) or
+  // the fully connected tiling the cap costs 15-17 %.  Unused dynamic LDS
+  // reserves the room.
+  const bool cap = bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16 && (p.nw == 1 || p.L >= 2);
+  p.lds = cap ? int32_t(163840 / 3 + 256) : 0;
   return p;
 }
 
@@ -282,7 +294,7 @@ void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* a
   s->K = int32_t(c->ckpt_every < c->T ? c->ckpt_every : c->T);
   s->nck = p.nck;
   s->beta = c->beta; s->vth = c->v_th;
-  s->mode = p.mode; s->ways = p.ways; s->pb = p.pb; s->tpc = p.tpc; s->cpt = p.cpt;
+  s->mode = p.mode; s->ways = p.ways; s->pb = p.pb; s->tpc = p.tpc; s->cpt = p.cpt; s->nw = p.nw;
   s->bpg = p.bpg; s->ntiles = p.ntiles;
 }
 

@@ -34,6 +34,7 @@ struct Plan {
   int32_t KS;     // backward stash capacity in steps (compile-time in the kernel)
   int32_t nck;    // interior checkpoints, ceil(T / K) - 1
   int32_t lds;    // dynamic LDS bytes per block, reserved only to cap blocks per CU
+  int32_t nw;     // neurons per lane and batch item in spatial tiles (1, or 2 in the backward)
 };
 
 struct ScanArgs {
@@ -50,6 +51,7 @@ struct ScanArgs {
   float beta, vth;
   float rP;             // 1 / P (residual dendrite)
   int32_t mode, ways, pb, tpc, cpt, bpg;
+  int32_t nw;           // spatial tiles: a lane takes positions p and p + 64 / L (nw = 2)
   int64_t ntiles;
 };
 

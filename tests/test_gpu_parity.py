@@ -86,6 +86,31 @@ def test_shapes(gpu_device, shape, variant):
     compare(case, run_gpu(case, gpu_device))
 
 
+# --- four-step spatial backward with two positions per lane (whole tiles) ---
+NW2_SHAPES = [
+    # T, batch, C, S, B, k, io
+    (4, 3, 5, 256, 8, 1, "f32"),
+    (4, 2, 3, 1024, 4, 1, "bf16"),
+    (4, 5, 2, 512, 16, 1, "f32"),
+    (4, 2, 4, 512, 2, 2, "f32"),
+    (4, 3, 2, 1024, 8, 1, "bf16"),
+    (4, 2, 3, 256, 32, 1, "f32"),
+]
+
+
+@pytest.mark.parametrize("shape", NW2_SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}k{}{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "res-id-atan-stateless-plif"])
+def test_two_positions_per_lane(gpu_device, shape, variant):
+    T, batch, C, S, B, k, io = shape
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, comps_per_branch=k, io=io,
+            psi="identity" if "-id-" in f"-{variant}-" else "mexhat", sg="sigmoid" if "sig" in variant else "atan",
+            stateful="stateless" not in variant, residual=variant.startswith("res"), beta=0.7)
+    seed = zlib.crc32(repr((shape, variant, "nw2")).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6, mask_rho=0.5 if "mask" in variant else None,
+                     name=f"nw2/{shape}/{variant}", beta_dev=0.8 if "plif" in variant else None, with_gv=True)
+    compare(case, run_gpu(case, gpu_device))
+
+
 # --- several compartments per branch (L2 norm over a branch's compartments) ---
 KC_SHAPES = [
     # T, batch, C, S, B, k, io, K
