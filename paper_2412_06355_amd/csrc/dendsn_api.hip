@@ -210,13 +210,19 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   p.nw = 1;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
-    // The four-step backward over whole tiles of 16-byte lane rows takes two
-    // positions per lane and item (a wave then reads 2 x 64 / L adjacent
-    // positions per row): measured 3-9 % faster on the fp32 conv layers, and
-    // 2 % slower with the 8-byte rows of bf16.
-    if (bwd && c->T == 4 && !p.cm && p.BL * p.KC * esz == 16 && c->S % (2 * p.pb) == 0) {
-      p.nw = 2;
-      p.pb *= 2;
+    // The four-step backward over whole tiles of 16-byte lane rows takes nw
+    // positions per lane and item, so a wave reads and writes nw x 64 / L
+    // adjacent positions (nw KiB) per row.  Measured on MI355X: nw = 4 when a
+    // neuron spans 2 or 4 lanes (cifar 911 -> 800 us against nw = 2, B = 16
+    // 885 -> 810 us; nw = 8 is slower again), nw = 2 with one lane per neuron
+    // (3-9 % faster than 1; 4 no better), and 2 for the channel-major layout with
+    // one lane per neuron (464 -> 435 us; with more lanes it lost 1 %).  bf16
+    // 8-byte rows lost 2 % and keep one position per lane.
+    int nw = p.cm ? (L == 1 ? 2 : 1) : (L == 1 ? 2 : 4);
+    while (nw > 1 && c->S % (nw * p.pb) != 0) nw /= 2;
+    if (bwd && c->T == 4 && p.BL * p.KC * esz == 16 && nw > 1) {
+      p.nw = nw;
+      p.pb *= nw;
     }
     p.tpc = int32_t(ceil_div(c->S, p.pb)); p.cpt = 1;
     p.ntiles = c->C * p.tpc;

@@ -505,11 +505,11 @@ __device__ __forceinline__ Pos locate(const ScanArgs& a) {
   const int tid = threadIdx.x;
   r.sub = tid % L;
   const int q = tid / L;
-  // nw = 2 (spatial tiles, backward): each wave covers 2 * 64 / L adjacent
-  // positions, a lane taking slot q of the first half and the same slot of the
-  // second, so each of the two accesses per row is contiguous across the wave.
+  // nw > 1 (spatial tiles, backward): each wave covers nw * 64 / L adjacent
+  // positions, a lane taking slot q of each 64 / L stretch, so each of the nw
+  // accesses per row is contiguous across the wave.
   constexpr int kSlots = 64 / L;
-  r.p = a.nw == 2 ? (q / kSlots) * (2 * kSlots) + q % kSlots : q % a.pb;
+  r.p = a.nw > 1 ? (q / kSlots) * (a.nw * kSlots) + q % kSlots : q % a.pb;
   // Batch ways are whole waves (kFC: pb * L == 64) or a single way, so the way
   // index is wave-uniform; readfirstlane lets the compiler keep it scalar.
   r.way = __builtin_amdgcn_readfirstlane(q / a.pb);
@@ -1013,22 +1013,28 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   const ScanArgs& a = ba.s;
   const float beta_r = ba.detach ? 0.0f : a.beta;
   const int64_t step = int64_t(a.ways) * a.M;  // neurons between this lane's items
-  // with nw = 2 a lane visits its two positions of each item in turn:
-  // neurons n, n + 64 / L, then the next item
-  const int64_t half = a.nw == 2 ? 64 / L : 0;
-  const int nvis = a.nw == 2 ? 2 * nk : nk;
-  int64_t n0 = bt0 * a.M;
+  // A lane visits its nw positions of each item in turn (neurons n, n + 64 / L,
+  // ...), then the next item.  n indexes the [T, N] rows; nx is the matching
+  // element offset of X / grad_x rows (n P, or in the channel-major layout the
+  // item's base plus the position shift).
+  const int nw = a.nw > 1 ? a.nw : 1;
+  const int64_t dn = 64 / L;                              // position shift inside an item
+  const int64_t dnx = kCM<V> ? dn : dn * a.P;
+  const int64_t dn_item = step - (nw - 1) * dn;           // last position -> next item
+  const int64_t dnx_item = step * a.P - (nw - 1) * dnx;
+  const int nvis = nw * nk;
+  int64_t n0 = bt0 * a.M, nx0 = bt0 * a.M * a.P;
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
   ChunkIn<E, KS> cur;
-  if (nvis > 0) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + n0 * a.P, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
+  if (nvis > 0) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
   float zero[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) zero[j] = 0.0f;
-  for (int i = 0; i < nvis; ++i) {
+  for (int i = 0, w = 0; i < nvis; ++i) {
     BwdLane<IO, E> bl;
-    bl.xbase = x + n0 * a.P;
-    bl.gxbase = static_cast<IO*>(ba.gx) + n0 * a.P;
+    bl.xbase = x + nx0;
+    bl.gxbase = static_cast<IO*>(ba.gx) + nx0;
     bl.gsbase = g + n0;
     bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
     bl.dh_next = 0.0f;
@@ -1037,11 +1043,14 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
     Stash<BL, KS, V> st;
     recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
     ChunkIn<E, KS> nxt;
-    const int64_t n1 = (half != 0 && (i & 1) == 0) ? n0 + half : n0 - half + step;
-    if (i + 1 < nvis) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + n1 * a.P, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
+    const bool last_w = ++w == nw;
+    if (last_w) w = 0;
+    const int64_t n1 = n0 + (last_w ? dn_item : dn), nx1 = nx0 + (last_w ? dnx_item : dnx);
+    if (i + 1 < nvis) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + nx1, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
     reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
     cur = nxt;
     n0 = n1;
+    nx0 = nx1;
   }
 }
 

@@ -95,6 +95,8 @@ NW2_SHAPES = [
     (4, 2, 4, 512, 2, 2, "f32"),
     (4, 3, 2, 1024, 8, 1, "bf16"),
     (4, 2, 3, 256, 32, 1, "f32"),
+    (4, 3, 2, 1024, 8, 1, "f32"),      # four positions per lane
+    (4, 2, 2, 512, 4, 4, "f32"),
 ]
 
 
@@ -196,6 +198,8 @@ CM_SHAPES = [
     (4, 2, 3, 300, 8, 2, "f32", 2),      # P = 16 over 4 lanes
     (6, 2, 5, 31, 4, 4, "bf16", 4),      # P = 16, k = 4, 4 lanes
     (4, 2, 2, 400, 7, 1, "f32", 4),      # odd branch count, one lane
+    (4, 3, 3, 512, 2, 2, "f32", 4),      # two positions per lane in the backward
+    (4, 2, 2, 1024, 4, 1, "f32", 4),
 ]
 
 

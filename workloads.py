@@ -85,6 +85,7 @@ WORKLOADS = {
                              alpha=0.8, beta=0.9, ckpt_every=8),
     # Task-incremental fully connected layer with a per-task branch-gating mask.
     "dbg": Workload("dbg", T=4, batch=64, C=8192, S=1, B=32, tasks=10, mask_rho=0.5),
+    "cifar_b16": Workload("cifar_b16", T=4, batch=64, C=128, S=32 * 32, B=16, x_std=0.5),
     # The CIFAR-shaped layer with bf16 storage.
     "cifar_bf16": Workload("cifar_bf16", T=4, batch=128, C=128, S=32 * 32, B=8, x_std=0.5, io="bf16"),
     # The paper's common dendrite (P = 4 compartments on B = 2 branches) on the
