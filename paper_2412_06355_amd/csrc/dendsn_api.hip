@@ -210,20 +210,28 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   p.nw = 1;
   if (c->S >= kThreads / L) {
     p.mode = kSpatial; p.ways = 1; p.pb = kThreads / L;
-    // The four-step backward over whole tiles of 16-byte lane rows takes nw
-    // positions per lane and item, so a wave reads and writes nw x 64 / L
-    // adjacent positions (nw KiB) per row.  Measured on MI355X: nw = 4 when a
-    // neuron spans 2 or 4 lanes (cifar 911 -> 800 us against nw = 2, B = 16
+    // A lane may take nw positions per batch item, so a wave reads and writes
+    // nw x 64 / L adjacent positions per row (fewer, longer-lived waves).
+    // Measured on MI355X.  Backward (four steps, 16-byte lane rows): nw = 4 when
+    // a neuron spans 2 or 4 lanes (cifar 911 -> 800 us against nw = 2, B = 16
     // 885 -> 810 us; nw = 8 is slower again), nw = 2 with one lane per neuron
     // (3-9 % faster than 1; 4 no better), and 2 for the channel-major layout with
-    // one lane per neuron (464 -> 435 us; with more lanes it lost 1 %).  bf16
-    // 8-byte rows lost 2 % and keep one position per lane.
-    int nw = p.cm ? (L == 1 ? 2 : 1) : (L == 1 ? 2 : 4);
-    while (nw > 1 && c->S % (nw * p.pb) != 0) nw /= 2;
-    if (bwd && c->T == 4 && p.BL * p.KC * esz == 16 && nw > 1) {
-      p.nw = nw;
-      p.pb *= nw;
+    // one lane per neuron (464 -> 435 us; with more lanes it lost 1 %); bf16
+    // 8-byte rows lost 2 %.  Forward: nw = 4 when a neuron spans several lanes
+    // (cifar 411 -> 395 us), 2 for fp32 with one lane per neuron (P = 4 on B = 2:
+    // 209 -> 199 us; 4 no better); one-lane bf16 neurons and channel-major
+    // neurons over several lanes gained nothing and keep 1.
+    int nw = 1;
+    if (bwd) {
+      if (c->T == 4 && p.BL * p.KC * esz == 16) nw = p.cm ? (L == 1 ? 2 : 1) : (L == 1 ? 2 : 4);
+    } else if (L >= 2) {
+      nw = p.cm ? 1 : 4;
+    } else if (esz == 4) {
+      nw = 2;
     }
+    while (nw > 1 && c->S % (nw * p.pb) != 0) nw /= 2;
+    p.nw = nw;
+    p.pb *= nw;
     p.tpc = int32_t(ceil_div(c->S, p.pb)); p.cpt = 1;
     p.ntiles = c->C * p.tpc;
   } else if (c->S == 1) {
@@ -237,10 +245,10 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   }
   // Batch groups (measured on MI355X): the backward wants ~16K waves in the grid
   // (more groups mean more partial sums to reduce); the forward over conv
-  // layers does best with about four batch items per lane.
+  // layers does best with about four neurons (batch items x positions) per lane.
   const int64_t target_waves = 16384;
   int64_t G = ceil_div(target_waves, p.ntiles * 4);
-  if (!bwd && p.mode == kSpatial) G = ceil_div(c->batch, 4);
+  if (!bwd && p.mode == kSpatial) G = ceil_div(c->batch * p.nw, 4);
   G = G < 1 ? 1 : G;
   const int64_t max_g = ceil_div(c->batch, p.ways);
   if (G > max_g) G = max_g;

@@ -562,6 +562,26 @@ __device__ __forceinline__ int items_of(const ScanArgs& a, const Pos& pos, int64
   return *first < end ? int((end - *first + a.ways - 1) / a.ways) : 0;
 }
 
+// A lane's walk over its neurons when it holds nw > 1 positions per batch item
+// (neurons n, n + 64 / L, ... of the item, then the next item): the wave-uniform
+// shifts of the [T, N] row index n and of the matching X element offset nx (n P,
+// or in the channel-major layout the item's base plus the position shift).
+struct Walk {
+  int nw;
+  int64_t dn, dnx, dn_item, dnx_item;
+};
+
+template <int L, bool CM>
+__device__ __forceinline__ Walk make_walk(const ScanArgs& a, int64_t item_neurons) {
+  Walk k;
+  k.nw = a.nw > 1 ? a.nw : 1;
+  k.dn = 64 / L;
+  k.dnx = CM ? k.dn : k.dn * a.P;
+  k.dn_item = item_neurons - (k.nw - 1) * k.dn;
+  k.dnx_item = item_neurons * a.P - (k.nw - 1) * k.dnx;
+  return k;
+}
+
 // ---------------------------------------------------------------------------
 // Forward kernel.
 //
@@ -574,12 +594,12 @@ __device__ __forceinline__ int items_of(const ScanArgs& a, const Pos& pos, int64
 template <typename IO, int BL, int D>
 struct RowCursor {  // wave-uniform position of the next chunk to load
   const IO* base;   // X row 0 of the current neuron's batch item
-  int k, t;         // neuron index in the lane's list, first row of the chunk
+  int w, t;         // position index inside the item (0 .. nw-1), first row of the chunk
 };
 
 template <bool CM, typename IO, int BL, int D>
 __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, D>& cur, uint32_t ox, int T,
-                                           int Tp, int64_t rowX, int64_t item_stride, float (&buf)[D][BL]) {
+                                           int Tp, int64_t rowX, const Walk& wk, float (&buf)[D][BL]) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = min(cur.t + k, T - 1);
@@ -588,8 +608,9 @@ __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, 
   cur.t += D;
   if (cur.t >= Tp) {
     cur.t = 0;
-    cur.k += 1;
-    cur.base += item_stride;
+    const bool last = ++cur.w == wk.nw;
+    if (last) cur.w = 0;
+    cur.base += last ? wk.dnx_item : wk.dnx;
   }
 }
 
@@ -601,6 +622,7 @@ struct FwdLane {
   float h;
   bool s;
   int t;          // step index of the chunk being computed (0 .. Tp-1)
+  int w;          // position index inside the batch item (0 .. nw-1)
   int kc;         // steps until the next checkpoint
   IO* sp;         // spikes row t of this batch item
   float* vp;      // v_soma row t (or null)
@@ -625,7 +647,7 @@ __device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, Fw
 
 template <typename IO, int BL, int L, int V, int D>
 __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
-                                              float alpha, bool lead, int T, int Tp, int64_t item_neurons,
+                                              float alpha, bool lead, int T, int Tp, const Walk& wk,
                                               const float (&buf)[D][BL * kKC<V>], FwdLane<IO, BL * kKC<V>>& st) {
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = fa.s;
@@ -653,8 +675,10 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
     }
   }
   st.t += D;
-  if (st.t >= Tp) {  // next batch item of this lane
-    const int64_t n0 = (st.sp - static_cast<IO*>(fa.spikes)) - int64_t(T) * a.N + item_neurons;
+  if (st.t >= Tp) {  // next neuron of this lane: next position of the item, or the next item
+    const bool last = ++st.w == wk.nw;
+    if (last) st.w = 0;
+    const int64_t n0 = (st.sp - static_cast<IO*>(fa.spikes)) - int64_t(T) * a.N + (last ? wk.dn_item : wk.dn);
     fwd_item_start<IO, E>(fa, n0, st);
   }
 }
@@ -677,23 +701,24 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   const int64_t rowX = a.N * a.P;
   int64_t bt0;
   const int nk = items_of(a, pos, &bt0);
-  const int nchunks = nk * (Tp / D);
-  const int64_t item_neurons = int64_t(a.ways) * a.M;
+  const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
+  const int nchunks = nk * wk.nw * (Tp / D);
 
   RowCursor<IO, E, D> cur;
   cur.base = static_cast<const IO*>(a.x) + bt0 * a.M * a.P;
-  cur.k = 0;
+  cur.w = 0;
   cur.t = 0;
   FwdLane<IO, E> st;
+  st.w = 0;
   fwd_item_start<IO, E>(fa, bt0 * a.M, st);
 
   float bufA[D][E], bufB[D][E];
-  if (nchunks > 0) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
+  if (nchunks > 0) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
   for (int c = 0; c < nchunks; c += 2) {
-    if (c + 1 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufB);
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufA, st);
-    if (c + 2 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, item_neurons * a.P, bufA);
-    if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, item_neurons, bufB, st);
+    if (c + 1 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
+    if (c + 2 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
+    if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
   }
 }
 

@@ -113,6 +113,32 @@ def test_two_positions_per_lane(gpu_device, shape, variant):
     compare(case, run_gpu(case, gpu_device))
 
 
+# --- the forward with several positions per lane and batch item, any length ---
+FWD_NW_SHAPES = [
+    # T, batch, C, S, B, k, io, K, layout, batch_groups
+    (7, 3, 2, 1024, 8, 1, "f32", 3, "npb", 0),       # 4 positions over 2 lanes, padded chunk, checkpoints
+    (5, 5, 2, 512, 4, 1, "f32", 2, "npb", 0),        # 2 positions, one lane; ragged batch groups
+    (6, 2, 3, 1024, 16, 1, "bf16", 4, "npb", 0),     # bf16 over 2 lanes
+    (9, 3, 2, 512, 2, 2, "f32", 4, "channel_major", 0),
+    (4, 6, 1, 2048, 8, 1, "f32", 4, "npb", 2),       # 3 batch items x 4 positions per lane
+    (3, 2, 2, 768, 8, 1, "f32", 2, "npb", 0),        # S = 768: 2 positions
+]
+
+
+@pytest.mark.parametrize("shape", FWD_NW_SHAPES, ids=lambda s: "T{}b{}C{}S{}B{}k{}{}K{}{}g{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig-mask", "res-id-atan-stateless-plif"])
+def test_forward_positions_per_lane(gpu_device, shape, variant):
+    T, batch, C, S, B, k, io, K, layout, groups = shape
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, comps_per_branch=k, io=io, ckpt_every=K, layout=layout,
+            batch_groups=groups, psi="identity" if "-id-" in f"-{variant}-" else "mexhat",
+            sg="sigmoid" if "sig" in variant else "atan", stateful="stateless" not in variant,
+            residual=variant.startswith("res"), beta=0.7)
+    seed = zlib.crc32(repr((shape, variant, "fwd-nw")).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6, mask_rho=0.5 if "mask" in variant else None,
+                     name=f"fwd-nw/{shape}/{variant}", beta_dev=0.8 if "plif" in variant else None, with_gv=True)
+    compare(case, run_gpu(case, gpu_device))
+
+
 # --- several compartments per branch (L2 norm over a branch's compartments) ---
 KC_SHAPES = [
     # T, batch, C, S, B, k, io, K
