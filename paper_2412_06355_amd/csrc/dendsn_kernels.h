@@ -184,6 +184,10 @@ __device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__bu
 // ---------------------------------------------------------------------------
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr int kAuxNT = 2;  // cache policy: non-temporal (streaming)
+// s_waitcnt vmcnt(0), other counters untouched: every vector memory access of
+// the wave has completed.
+constexpr int kWaitVmem = 0x0F70;
+
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
   // raw buffer, byte range 4 GiB - 1 (every lane offset is a uint32 below it)
@@ -343,6 +347,100 @@ __device__ __forceinline__ void store_gx(IO* row, uint32_t off, uint32_t es, con
 template <typename IO>
 __device__ __forceinline__ float load_row_one(const IO* row, uint32_t off) {
   return bload_one(make_rsrc(row), off, 0, row);
+}
+
+// ---------------------------------------------------------------------------
+// Rows in raw form: the dwords the loads return (fp32 elements, bf16 element
+// pairs, or one bf16 element in the low half), converted to float where they
+// are used, so that the wait for a prefetched row falls at its first use and not
+// right after its load.
+// ---------------------------------------------------------------------------
+template <typename IO, int E, bool CM>
+constexpr int kRawW = (sizeof(IO) == 2 && !CM && E % 2 == 0) ? E / 2 : E;  // dwords per row
+
+// Global (address) loads, as the forward issues them.
+template <typename IO, int E, bool CM, int W>
+__device__ __forceinline__ void load_raw(const IO* row, uint32_t off, uint32_t es, uint32_t (&w)[W]) {
+  constexpr bool dwords = sizeof(IO) == 4 || (!CM && W * 2 == E);  // contiguous whole dwords
+  if constexpr (CM) {
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      const IO* q = at(row, off + uint32_t(i) * es);
+      if constexpr (sizeof(IO) == 4) w[i] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(q));
+      else w[i] = uint32_t(__builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(q)));
+    }
+  } else if constexpr (dwords && W % 4 == 0) {
+    const u32x4_t* q = reinterpret_cast<const u32x4_t*>(at(row, off));
+#pragma unroll
+    for (int i = 0; i < W / 4; ++i) {
+      const u32x4_t v = __builtin_nontemporal_load(q + i);
+      w[4 * i] = v.x; w[4 * i + 1] = v.y; w[4 * i + 2] = v.z; w[4 * i + 3] = v.w;
+    }
+  } else if constexpr (dwords && W % 2 == 0) {
+    const u32x2_t* q = reinterpret_cast<const u32x2_t*>(at(row, off));
+#pragma unroll
+    for (int i = 0; i < W / 2; ++i) {
+      const u32x2_t v = __builtin_nontemporal_load(q + i);
+      w[2 * i] = v.x; w[2 * i + 1] = v.y;
+    }
+  } else if constexpr (dwords) {
+    const uint32_t* q = reinterpret_cast<const uint32_t*>(at(row, off));
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = __builtin_nontemporal_load(q + i);
+  } else {
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(at(row, off));
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = uint32_t(__builtin_nontemporal_load(q + i));
+  }
+}
+
+// Buffer loads, as the backward issues them.
+template <typename IO, int E, bool CM, int W>
+__device__ __forceinline__ void bload_raw(rsrc_t r, uint32_t off, uint32_t es, uint32_t (&w)[W]) {
+  constexpr bool dwords = sizeof(IO) == 4 || (!CM && W * 2 == E);  // contiguous whole dwords
+  if constexpr (CM) {
+#pragma unroll
+    for (int i = 0; i < W; ++i)
+      w[i] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(r, off, uint32_t(i) * es, kAuxNT)
+                             : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, uint32_t(i) * es, kAuxNT));
+  } else if constexpr (dwords && W % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < W / 4; ++i) {
+      const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16u * i, 0, kAuxNT);
+      w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+    }
+  } else if constexpr (dwords && W % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < W / 2; ++i) {
+      const u32x2_t q = __builtin_amdgcn_raw_buffer_load_b64(r, off + 8u * i, 0, kAuxNT);
+      w[2 * i] = q.x; w[2 * i + 1] = q.y;
+    }
+  } else if constexpr (dwords) {
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = __builtin_amdgcn_raw_buffer_load_b32(r, off + 4u * i, 0, kAuxNT);
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off + 2u * i, 0, kAuxNT));
+  }
+}
+
+template <typename IO, int E, int W>
+__device__ __forceinline__ void raw_to_float(const uint32_t (&w)[W], float (&v)[E]) {
+  if constexpr (sizeof(IO) == 4) {
+#pragma unroll
+    for (int i = 0; i < E; ++i) v[i] = __uint_as_float(w[i]);
+  } else if constexpr (W * 2 == E) {
+#pragma unroll
+    for (int i = 0; i < W; ++i) { v[2 * i] = bf16_lo(w[i]); v[2 * i + 1] = bf16_hi(w[i]); }
+  } else {
+#pragma unroll
+    for (int i = 0; i < E; ++i) v[i] = bf16_lo(w[i]);
+  }
+}
+
+template <typename IO>
+__device__ __forceinline__ float raw_to_float(uint32_t w) {
+  return sizeof(IO) == 4 ? __uint_as_float(w) : bf16_lo(w);
 }
 
 __device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
@@ -599,11 +697,12 @@ struct RowCursor {  // wave-uniform position of the next chunk to load
 
 template <bool CM, typename IO, int BL, int D>
 __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, D>& cur, uint32_t ox, int T,
-                                           int Tp, int64_t rowX, const Walk& wk, float (&buf)[D][BL]) {
+                                           int Tp, int64_t rowX, const Walk& wk,
+                                           uint32_t (&buf)[D][kRawW<IO, BL, CM>]) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = min(cur.t + k, T - 1);
-    load_x<BL, CM, false>(cur.base + int64_t(t) * rowX, ox, a.xes, buf[k]);
+    load_raw<IO, BL, CM>(cur.base + int64_t(t) * rowX, ox, a.xes, buf[k]);
   }
   cur.t += D;
   if (cur.t >= Tp) {
@@ -648,13 +747,16 @@ __device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, Fw
 template <typename IO, int BL, int L, int V, int D>
 __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, bool lead, int T, int Tp, const Walk& wk,
-                                              const float (&buf)[D][BL * kKC<V>], FwdLane<IO, BL * kKC<V>>& st) {
+                                              const uint32_t (&buf)[D][kRawW<IO, BL * kKC<V>, kCM<V>>],
+                                              FwdLane<IO, BL * kKC<V>>& st) {
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = fa.s;
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = st.t + k;
-    const float z = dendrite_step<BL, L, V>(st.vd, buf[k], br, alpha);
+    float xk[E];
+    raw_to_float<IO, E>(buf[k], xk);
+    const float z = dendrite_step<BL, L, V>(st.vd, xk, br, alpha);
     soma_step(st.h, st.s, z, a.beta, a.vth);
     if (t < T) {  // padded steps store nothing
       if (lead) {
@@ -712,13 +814,25 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   st.w = 0;
   fwd_item_start<IO, E>(fa, bt0 * a.M, st);
 
-  float bufA[D][E], bufB[D][E];
-  if (nchunks > 0) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
-  for (int c = 0; c < nchunks; c += 2) {
-    if (c + 1 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
+  if (nchunks <= 0) return;
+  uint32_t bufA[D][kRawW<IO, E, kCM<V>>], bufB[D][kRawW<IO, E, kCM<V>>];
+  load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
+  // Every later wait is then counted from loads issued inside the loop, which
+  // are unconditional (the last one or two chunks run after it).
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+  int c = 0;
+  for (; c + 2 < nchunks; c += 2) {
+    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
     compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
-    if (c + 2 < nchunks) load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
-    if (c + 1 < nchunks) compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
+    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
+  }
+  if (c + 1 < nchunks) {
+    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
+  } else {
+    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
   }
 }
 
@@ -781,6 +895,37 @@ __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& 
     in.gs[k] = load_row_one(gsbase + t * a.N, lo.s);
   }
   load_chunk_gv<E, CS>(a, lo, gvbase, c0, in);
+}
+
+// A chunk's rows in raw form (see load_raw).  The single-chunk pipeline
+// carries the next neuron's rows this way: a conversion issued next to the
+// loads would make the wave wait for them at once instead of while the current
+// neuron's adjoint pass runs.
+template <typename IO, int E, int CS, bool CM>
+struct ChunkRaw {
+  uint32_t x[CS][kRawW<IO, E, CM>];
+  uint32_t gs[CS];
+  float gv[CS];
+};
+
+template <typename IO, int E, int CS, bool CM>
+__device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
+                                               const IO* gsbase, const float* gvbase, ChunkRaw<IO, E, CS, CM>& in) {
+  const int64_t rowX = a.N * a.P;
+#pragma unroll
+  for (int k = 0; k < CS; ++k) {
+    bload_raw<IO, E, CM>(make_rsrc(xbase + k * rowX), lo.x, a.xes, in.x[k]);
+    const rsrc_t rg = make_rsrc(gsbase + k * a.N);
+    in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, lo.s, 0, kAuxNT)
+                               : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, lo.s, 0, kAuxNT));
+  }
+  if (gvbase) {
+#pragma unroll
+    for (int k = 0; k < CS; ++k) in.gv[k] = __builtin_nontemporal_load(at(gvbase + int64_t(k) * a.N, lo.v));
+  } else {
+#pragma unroll
+    for (int k = 0; k < CS; ++k) in.gv[k] = 0.0f;
+  }
 }
 
 // The checkpointed state a segment starts from.
@@ -1051,32 +1196,45 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   int64_t n0 = bt0 * a.M, nx0 = bt0 * a.M * a.P;
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
-  ChunkIn<E, KS> cur;
-  if (nvis > 0) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, 0, cur);
-  float zero[E];
-#pragma unroll
-  for (int j = 0; j < E; ++j) zero[j] = 0.0f;
-  for (int i = 0, w = 0; i < nvis; ++i) {
+  if (nvis <= 0) return;
+  ChunkRaw<IO, E, KS, kCM<V>> cur;
+  load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, cur);
+  // Every later wait is then counted from loads issued inside the loop, whose
+  // next-neuron loads are unconditional (the last neuron runs after it).
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+  int w = 0;
+  auto item = [&](const ChunkRaw<IO, E, KS, kCM<V>>& in, bool more, ChunkRaw<IO, E, KS, kCM<V>>& nxt) {
     BwdLane<IO, E> bl;
     bl.xbase = x + nx0;
     bl.gxbase = static_cast<IO*>(ba.gx) + nx0;
     bl.gsbase = g + n0;
     bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
     bl.dh_next = 0.0f;
+    float xin[KS][E], gsv[KS], zero[E];
 #pragma unroll
-    for (int j = 0; j < E; ++j) bl.lam[j] = 0.0f;
+    for (int j = 0; j < E; ++j) { bl.lam[j] = 0.0f; zero[j] = 0.0f; }
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      raw_to_float<IO, E>(in.x[k], xin[k]);
+      gsv[k] = raw_to_float<IO>(in.gs[k]);
+    }
     Stash<BL, KS, V> st;
-    recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, cur.x, st);
-    ChunkIn<E, KS> nxt;
-    const bool last_w = ++w == nw;
-    if (last_w) w = 0;
-    const int64_t n1 = n0 + (last_w ? dn_item : dn), nx1 = nx0 + (last_w ? dnx_item : dnx);
-    if (i + 1 < nvis) load_chunk_in<IO, E, KS, kCM<V>>(a, lo, x + nx1, g + n1, ba.gv ? ba.gv + n1 : nullptr, 0, nxt);
-    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, cur.gs, cur.gv, bl, acc);
+    recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, xin, st);
+    if (more) {
+      const bool last_w = ++w == nw;
+      if (last_w) w = 0;
+      n0 += last_w ? dn_item : dn;
+      nx0 += last_w ? dnx_item : dnx;
+      load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, nxt);
+    }
+    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, in.gv, bl, acc);
+  };
+  for (int i = 0; i + 1 < nvis; ++i) {
+    ChunkRaw<IO, E, KS, kCM<V>> nxt;
+    item(cur, true, nxt);
     cur = nxt;
-    n0 = n1;
-    nx0 = nx1;
   }
+  item(cur, false, cur);
 }
 
 // Per channel the backward produces W = 2 B + P parameter gradients, in the
