@@ -18,21 +18,14 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdendsn.so")
 
-SOURCES = [
-    "dendsn_fwd_f32_cm.hip",
-    "dendsn_fwd_bf16_cm.hip",
-    "dendsn_bwd_f32_cm.hip",
-    "dendsn_bwd_bf16_cm.hip",
-    "dendsn_fwd_f32_kc.hip",
-    "dendsn_fwd_bf16_kc.hip",
-    "dendsn_bwd_f32_kc.hip",
-    "dendsn_bwd_bf16_kc.hip",
-    "dendsn_api.hip",
-    "dendsn_fwd_f32.hip",
-    "dendsn_fwd_bf16.hip",
-    "dendsn_bwd_f32.hip",
-    "dendsn_bwd_bf16.hip",
-]
+# (source, extra flags, object name).  The backward units compile once per
+# surrogate derivative (-DDENDSN_SG=0: atan, 1: sigmoid); the heaviest first.
+_BWD = ["dendsn_bwd_bf16.hip", "dendsn_bwd_bf16_kc.hip", "dendsn_bwd_f32.hip", "dendsn_bwd_f32_kc.hip",
+        "dendsn_bwd_f32_cm.hip", "dendsn_bwd_bf16_cm.hip"]
+_OTHER = ["dendsn_fwd_f32_cm.hip", "dendsn_fwd_bf16_cm.hip", "dendsn_fwd_f32_kc.hip", "dendsn_fwd_bf16_kc.hip",
+          "dendsn_api.hip", "dendsn_fwd_f32.hip", "dendsn_fwd_bf16.hip"]
+SOURCES = [(src, [f"-DDENDSN_SG={k}"], f"{src[:-4]}_sg{k}.o") for src in _BWD for k in (0, 1)] + \
+          [(src, [], f"{src[:-4]}.o") for src in _OTHER]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -53,9 +46,10 @@ CFLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(unit) -> str:
+    src, extra, name = unit
+    obj = os.path.join(BUILD, name)
+    cmd = [HIPCC, *CFLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -12,16 +12,22 @@ namespace dendsn {
 
 hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream);
 hipError_t launch_fwd_bf16(const Plan& pl, const FwdArgs& fa, int psi, hipStream_t stream);
-hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
-hipError_t launch_bwd_bf16(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_bwd_f32_sg0(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_bwd_f32_sg1(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_bwd_bf16_sg0(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
+hipError_t launch_bwd_bf16_sg1(const Plan& pl, const BwdArgs& ba, int psi, hipStream_t stream);
 hipError_t launch_fwd_f32_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
 hipError_t launch_fwd_bf16_kc(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
-hipError_t launch_bwd_f32_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
-hipError_t launch_bwd_bf16_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_kc_sg0(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_kc_sg1(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_kc_sg0(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_kc_sg1(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
 hipError_t launch_fwd_f32_cm(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
 hipError_t launch_fwd_bf16_cm(const Plan& pl, const FwdArgs& fa, int v, hipStream_t stream);
-hipError_t launch_bwd_f32_cm(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
-hipError_t launch_bwd_bf16_cm(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_cm_sg0(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_f32_cm_sg1(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_cm_sg0(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
+hipError_t launch_bwd_bf16_cm_sg1(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream);
 
 // Fixed-order float64 sums of the per-block partials into the parameter
 // gradients.  Outputs o = c * W + ol with W = 2 B + P: ol < B is g_kappa of
@@ -424,6 +430,10 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   ba.ckpt = ckpt;
   ba.gspk = grad_spikes;
   ba.gv = grad_v_soma;
+  // the single-chunk pipeline reads grad_v_soma through a buffer of gvn bytes:
+  // with none, an empty buffer whose loads all return 0
+  ba.gvz = grad_v_soma ? grad_v_soma : static_cast<const float*>(grad_spikes);
+  ba.gvn = grad_v_soma ? 0xFFFFFFFFu : 0u;
   ba.gx = grad_x;
   ba.wsP = static_cast<float*>(workspace);
   ba.wsA = reinterpret_cast<float*>(static_cast<char*>(workspace) + offA);
@@ -431,14 +441,18 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   ba.slots = int64_t(p.G) * p.tpc;
   ba.wide = ba.slots > kNarrowSlots;
   ba.detach = cfg->detach_reset;
-  ba.sg = cfg->sg;
   ba.sg_scale = cfg->sg_scale;
   const int v = cfg->psi | (cfg->residual << 1);
   const bool bf = cfg->io == DENDSN_IO_BF16;
-  hipError_t e =
-      p.cm ? (bf ? launch_bwd_bf16_cm(p, ba, v, stream) : launch_bwd_f32_cm(p, ba, v, stream))
-      : p.KC == 1 ? (bf ? launch_bwd_bf16(p, ba, v, stream) : launch_bwd_f32(p, ba, v, stream))
-                  : (bf ? launch_bwd_bf16_kc(p, ba, v, stream) : launch_bwd_f32_kc(p, ba, v, stream));
+  hipError_t e;
+  if (cfg->sg == DENDSN_SG_SIGMOID)
+    e = p.cm ? (bf ? launch_bwd_bf16_cm_sg1(p, ba, v, stream) : launch_bwd_f32_cm_sg1(p, ba, v, stream))
+        : p.KC == 1 ? (bf ? launch_bwd_bf16_sg1(p, ba, v, stream) : launch_bwd_f32_sg1(p, ba, v, stream))
+                    : (bf ? launch_bwd_bf16_kc_sg1(p, ba, v, stream) : launch_bwd_f32_kc_sg1(p, ba, v, stream));
+  else
+    e = p.cm ? (bf ? launch_bwd_bf16_cm_sg0(p, ba, v, stream) : launch_bwd_f32_cm_sg0(p, ba, v, stream))
+        : p.KC == 1 ? (bf ? launch_bwd_bf16_sg0(p, ba, v, stream) : launch_bwd_f32_sg0(p, ba, v, stream))
+                    : (bf ? launch_bwd_bf16_kc_sg0(p, ba, v, stream) : launch_bwd_f32_kc_sg0(p, ba, v, stream));
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("backward launch: ") + hipGetErrorString(e));
 
   FinArgs f;

@@ -1,23 +1,30 @@
 // Backward-kernel instantiations and dispatch for bf16 storage with KC = 2 or 4
 // compartments per branch (stash capacity 4).  V: bit 0 = Mexican-hat
-// activation, bit 1 = residual dendrite, bits 2-3 = log2(KC).
+// activation, bit 1 = residual dendrite, bits 2-3 = log2(KC), bit 5 = sigmoid
+// surrogate (DENDSN_SG).
 #include "dendsn_kernels.h"
 
+#ifndef DENDSN_SG
+#error "compile once per surrogate: -DDENDSN_SG=0 (atan) or 1 (sigmoid)"
+#endif
+
 namespace dendsn {
+
+constexpr int kVS = DENDSN_SG << 5;  // surrogate bit of the variant
 
 template <int BL, int L, int KC>
 static hipError_t launch_bwd_kc_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = (KC == 2 ? 1 : 2) << 2;
   switch (v & 3) {
-    case 0: dendsn_bwd_kernel<bf16_t, BL, L, VK | 0, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<bf16_t, BL, L, VK | 1, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<bf16_t, BL, L, VK | 2, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<bf16_t, BL, L, VK | 3, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 0: dendsn_bwd_kernel<bf16_t, BL, L, kVS | VK | 0, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 1: dendsn_bwd_kernel<bf16_t, BL, L, kVS | VK | 1, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 2: dendsn_bwd_kernel<bf16_t, BL, L, kVS | VK | 2, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 3: dendsn_bwd_kernel<bf16_t, BL, L, kVS | VK | 3, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_bf16_kc(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream) {
+hipError_t DENDSN_SG_NAME(launch_bwd_bf16_kc)(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
   if (pl.KS != 4) return hipErrorInvalidValue;
 #define DENDSN_FAST_CASE(BL_, L_, KC_) \

@@ -1,22 +1,29 @@
 // Backward-kernel instantiations and dispatch for f32 storage.
-// V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite; KS: stash steps.
+// V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite,
+// bit 5 = sigmoid surrogate (DENDSN_SG); KS: stash steps.
 #include "dendsn_kernels.h"
 
+#ifndef DENDSN_SG
+#error "compile once per surrogate: -DDENDSN_SG=0 (atan) or 1 (sigmoid)"
+#endif
+
 namespace dendsn {
+
+constexpr int kVS = DENDSN_SG << 5;  // surrogate bit of the variant
 
 template <int BL, int L, int KS>
 static hipError_t launch_bwd_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
   switch (v) {
-    case 0: dendsn_bwd_kernel<float, BL, L, 0, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<float, BL, L, 1, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<float, BL, L, 2, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<float, BL, L, 3, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 0: dendsn_bwd_kernel<float, BL, L, kVS | 0, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 1: dendsn_bwd_kernel<float, BL, L, kVS | 1, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 2: dendsn_bwd_kernel<float, BL, L, kVS | 2, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    case 3: dendsn_bwd_kernel<float, BL, L, kVS | 3, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_f32(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream) {
+hipError_t DENDSN_SG_NAME(launch_bwd_f32)(const Plan& pl, const BwdArgs& ba, int v, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
 #define DENDSN_FAST_CASE(BL_, L_)                                                   \
   if (pl.BL == BL_ && pl.L == L_ && pl.fast) {                                      \

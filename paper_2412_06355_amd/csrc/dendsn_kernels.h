@@ -37,6 +37,7 @@ template <int V> constexpr bool kMH = (V & 1) != 0;
 template <int V> constexpr bool kRes = (V & 2) != 0;
 template <int V> constexpr int kKC = 1 << ((V >> 2) & 3);
 template <int V> constexpr bool kCM = (V & 16) != 0;
+template <int V> constexpr int kSG = (V >> 5) & 1;  // backward only: dendsn_sg surrogate
 
 // -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.721347520444481703680f;
@@ -192,6 +193,12 @@ constexpr int kWaitVmem = 0x0F70;
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
   // raw buffer, byte range 4 GiB - 1 (every lane offset is a uint32 below it)
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
+}
+
+// A raw buffer of `bytes` bytes: loads at or past the end return 0 without
+// touching memory (bytes = 0 makes every load a zero).
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
 }
 
 template <int BL>
@@ -577,7 +584,8 @@ __device__ __forceinline__ void soma_step(float& h, bool& s, float z, float beta
   s = h >= vth;                   // Theta(H - v_th), Theta(0) = 1
 }
 
-// Surrogate derivative of Theta at x = H - v_th.
+// Surrogate derivative of Theta at x = H - v_th; kind is a compile-time
+// constant of each backward kernel (dendsn_sg).
 __device__ __forceinline__ float surrogate(float x, int kind, float a) {
   if (kind == 1) {  // a sigma(a x) (1 - sigma(a x)) = a e / (1 + e)^2, e = exp(-|a x|)
     const float e = __builtin_amdgcn_exp2f(-fabsf(a * x) * kLog2e);
@@ -910,7 +918,8 @@ struct ChunkRaw {
 
 template <typename IO, int E, int CS, bool CM>
 __device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
-                                               const IO* gsbase, const float* gvbase, ChunkRaw<IO, E, CS, CM>& in) {
+                                               const IO* gsbase, const float* gvbase, uint32_t gvbytes,
+                                               ChunkRaw<IO, E, CS, CM>& in) {
   const int64_t rowX = a.N * a.P;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
@@ -919,13 +928,10 @@ __device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff&
     in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, lo.s, 0, kAuxNT)
                                : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, lo.s, 0, kAuxNT));
   }
-  if (gvbase) {
+  // grad_v_soma rows (a buffer of no bytes when absent: every load returns 0)
 #pragma unroll
-    for (int k = 0; k < CS; ++k) in.gv[k] = __builtin_nontemporal_load(at(gvbase + int64_t(k) * a.N, lo.v));
-  } else {
-#pragma unroll
-    for (int k = 0; k < CS; ++k) in.gv[k] = 0.0f;
-  }
+  for (int k = 0; k < CS; ++k)
+    in.gv[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(gvbase + int64_t(k) * a.N, gvbytes), lo.v, 0, kAuxNT));
 }
 
 // The checkpointed state a segment starts from.
@@ -997,7 +1003,7 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
   for (int k = CS - 1; k >= 0; --k) {
     const float hk = st.h[k];
     const bool sk = hk >= vth;
-    const float sgv = surrogate(hk - vth, ba.sg, ba.sg_scale);
+    const float sgv = surrogate(hk - vth, kSG<V>, ba.sg_scale);
     const float dS = fmaf(-beta_r * hk, bl.dh_next, gs[k]);  // beta_r = 0: reset detached
     float dh = fmaf(sgv, dS, gvr[k]);
     dh = sk ? dh : fmaf(beta, bl.dh_next, dh);
@@ -1198,7 +1204,7 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   const IO* g = static_cast<const IO*>(ba.gspk);
   if (nvis <= 0) return;
   ChunkRaw<IO, E, KS, kCM<V>> cur;
-  load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, cur);
+  load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, cur);
   // Every later wait is then counted from loads issued inside the loop, whose
   // next-neuron loads are unconditional (the last neuron runs after it).
   __builtin_amdgcn_s_waitcnt(kWaitVmem);
@@ -1225,7 +1231,7 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
       if (last_w) w = 0;
       n0 += last_w ? dn_item : dn;
       nx0 += last_w ? dnx_item : dnx;
-      load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gv ? ba.gv + n0 : nullptr, nxt);
+      load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
     }
     reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, in.gv, bl, acc);
   };

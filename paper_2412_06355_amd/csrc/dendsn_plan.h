@@ -8,6 +8,13 @@ namespace dendsn {
 
 constexpr int kThreads = 256;  // 4 wave64s per block
 
+// The backward translation units are compiled once per surrogate derivative
+// (-DDENDSN_SG=0: atan, 1: sigmoid), which is bit 5 of the kernel variant V; their
+// launchers carry the suffix _sg0 / _sg1.
+#define DENDSN_SG_CAT2(name, k) name##_sg##k
+#define DENDSN_SG_CAT(name, k) DENDSN_SG_CAT2(name, k)
+#define DENDSN_SG_NAME(name) DENDSN_SG_CAT(name, DENDSN_SG)
+
 // How the positions m = c * S + s of one sample are cut into per-block tiles.
 // Tiles never straddle a channel unless they hold whole channels, so a block's
 // parameter-gradient partials belong to a known set of channels.
@@ -74,8 +81,9 @@ struct BwdArgs {
   int64_t slots;    // partial slots per output: G * tpc
   int32_t wide;     // 1: output-major layout (slots > kNarrowSlots)
   int32_t detach;
-  int32_t sg;
   float sg_scale;
+  const float* gvz;  // grad_v_soma, or any address when absent
+  uint32_t gvn;      // bytes readable through gvz: 0xffffffff, or 0 when absent
 };
 
 struct FinArgs {
