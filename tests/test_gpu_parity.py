@@ -399,8 +399,9 @@ def test_mask_of_ones_equals_no_mask(gpu_device):
         assert torch.equal(_bits(a["grads"][k]), _bits(b["grads"][k])), k
 
 
-def test_masked_branches_get_exact_positive_zero(gpu_device):
-    case = make_case(cfg(T=4, batch=2, C=64, S=3, B=8), seed=14, mask_rho=0.5, name="mask-zero")
+@pytest.mark.parametrize("io,S", [("f32", 3), ("bf16", 3), ("bf16", 512)])
+def test_masked_branches_get_exact_positive_zero(gpu_device, io, S):
+    case = make_case(cfg(T=4, batch=2, C=64, S=S, B=8, io=io), seed=14, mask_rho=0.5, name=f"mask-zero/{io}/S{S}")
     # gated-off branches receive inf / nan inputs: nothing may leak out of them
     cidx = (np.arange(case.cfg.N) // case.cfg.S) % case.cfg.C
     off = (case.mask == 0)[cidx]
