@@ -275,6 +275,17 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   // reserves the room.
   const bool cap = bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16 && (p.nw == 1 || p.L >= 2);
   p.lds = cap ? int32_t(163840 / 3 + 256) : 0;
+  // XCD runs (blocks are dealt to the 8 XCDs round-robin; measured on MI355X):
+  // fully connected tiles in runs of 32 blocks per XCD (dbg forward / backward
+  // -6 / -5 %, long horizon -5 / -3 %: neighbouring tiles share the cache lines
+  // of their spike and grad_spikes rows), the fp32 forward over conv tiles one
+  // contiguous eighth of the grid per XCD (cifar -4 %); otherwise round-robin
+  // (with runs the conv backward and the bf16 stem lost 1-5 %).
+  const int64_t nb = p.ntiles * p.G;
+  int64_t xk = 1;
+  if (p.mode == kFC) xk = 32;
+  else if (!bwd && p.mode == kSpatial && esz == 4) xk = nb / 8;
+  p.xk = (xk > 1 && nb % (8 * xk) == 0) ? int32_t(xk) : 1;
   return p;
 }
 
@@ -316,6 +327,7 @@ void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* a
   s->nck = p.nck;
   s->beta = c->beta; s->vth = c->v_th;
   s->mode = p.mode; s->ways = p.ways; s->pb = p.pb; s->tpc = p.tpc; s->cpt = p.cpt; s->nw = p.nw;
+  s->xk = p.xk;
   s->bpg = p.bpg; s->ntiles = p.ntiles;
 }
 

@@ -653,7 +653,14 @@ __device__ __forceinline__ Pos locate(const ScanArgs& a) {
   // Batch ways are whole waves (kFC: pb * L == 64) or a single way, so the way
   // index is wave-uniform; readfirstlane lets the compiler keep it scalar.
   r.way = __builtin_amdgcn_readfirstlane(q / a.pb);
-  const int64_t blk = blockIdx.x;
+  // Blocks are dealt to the 8 XCDs round-robin; with xk > 1 block b takes the
+  // tile of b's slot in runs of xk consecutive tiles per XCD turn, so tiles
+  // that share cache lines (and neighbouring DRAM pages) meet in one XCD's L2.
+  int64_t blk = blockIdx.x;
+  if (a.xk > 1) {
+    const int64_t x = blk % 8, j = blk / 8;
+    blk = (j / a.xk) * (8 * int64_t(a.xk)) + x * a.xk + j % a.xk;
+  }
   r.tile = blk % a.ntiles;
   r.g = int(blk / a.ntiles);
   if (a.mode == kSpatial) {

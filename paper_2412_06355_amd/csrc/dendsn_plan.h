@@ -41,7 +41,8 @@ struct Plan {
   int32_t KS;     // backward stash capacity in steps (compile-time in the kernel)
   int32_t nck;    // interior checkpoints, ceil(T / K) - 1
   int32_t lds;    // dynamic LDS bytes per block, reserved only to cap blocks per CU
-  int32_t nw;     // neurons per lane and batch item in spatial tiles (1, or 2 in the backward)
+  int32_t nw;     // positions per lane and batch item in spatial tiles (1, 2 or 4)
+  int32_t xk;     // XCD runs: consecutive tiles per XCD turn (1: plain round-robin)
 };
 
 struct ScanArgs {
@@ -58,7 +59,8 @@ struct ScanArgs {
   float beta, vth;
   float rP;             // 1 / P (residual dendrite)
   int32_t mode, ways, pb, tpc, cpt, bpg;
-  int32_t nw;           // spatial tiles: a lane takes positions p and p + 64 / L (nw = 2)
+  int32_t nw;           // spatial tiles: a lane takes positions p, p + 64 / L, ... (nw of them)
+  int32_t xk;           // runs of xk consecutive blocks share an XCD (see locate)
   int64_t ntiles;
 };
 
