@@ -256,6 +256,9 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   const int64_t target_waves = 16384;
   int64_t G = ceil_div(target_waves, p.ntiles * 4);
   if (!bwd && p.mode == kSpatial) G = ceil_div(c->batch * p.nw, esz == 2 ? 8 : 4);
+  // fully connected tiles (both directions): four batch items per wave (dbg: the
+  // same as ~16K waves; long horizon, T = 64: forward -5 %, backward -3 %)
+  if (p.mode == kFC) G = ceil_div(c->batch, int64_t(p.ways) * 4);
   G = G < 1 ? 1 : G;
   const int64_t max_g = ceil_div(c->batch, p.ways);
   if (G > max_g) G = max_g;
