@@ -23,7 +23,7 @@ hipError_t launch_fwd_bf16_cm(const Plan& pl, const FwdArgs& fa, int v, hipStrea
   if (!pl.cm) return hipErrorInvalidValue;
 #define DENDSN_CASE(BL_, L_, KC_) \
   if (pl.BL == BL_ && pl.L == L_ && pl.KC == KC_) return launch_fwd_cm_v<BL_, L_, KC_>(grid, fa, v, size_t(pl.lds), stream);
-  DENDSN_CM(DENDSN_CASE)
+  DENDSN_CM_FWD(DENDSN_CASE)
 #undef DENDSN_CASE
   return hipErrorInvalidValue;
 }

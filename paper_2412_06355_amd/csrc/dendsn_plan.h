@@ -136,5 +136,8 @@ constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread p
 #define DENDSN_CM(X) X(1, 1, 1) X(2, 1, 1) X(3, 1, 1) X(4, 1, 1) X(5, 1, 1) X(7, 1, 1) X(3, 2, 1) \
                      X(4, 2, 1) X(4, 4, 1) X(1, 1, 2) X(2, 1, 2) X(3, 1, 2) X(2, 2, 2) X(2, 4, 2) \
                      X(1, 1, 4) X(1, 2, 4) X(1, 4, 4)
+// The channel-major forward holds up to 8 compartments per lane: a power-of-two
+// backward split with half the lanes (the same balanced branch-sum tree).
+#define DENDSN_CM_FWD(X) DENDSN_CM(X) X(8, 1, 1) X(8, 2, 1) X(4, 1, 2) X(4, 2, 2) X(2, 1, 4) X(2, 2, 4)
 
 }  // namespace dendsn
