@@ -225,15 +225,16 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
     // Measured on MI355X.  Backward (four steps, 16-byte lane rows): nw = 4 when
     // a neuron spans 2 or 4 lanes (cifar 911 -> 800 us against nw = 2, B = 16
     // 885 -> 810 us; nw = 8 is slower again), nw = 2 with one lane per neuron
-    // (3-9 % faster than 1; 4 no better), and 2 for the channel-major layout with
-    // one lane per neuron (464 -> 435 us; with more lanes it lost 1 %); bf16
-    // 8-byte rows lost 2 %.  Forward: nw = 4 when a neuron spans several lanes
-    // (cifar 411 -> 395 us), 2 for fp32 with one lane per neuron (P = 4 on B = 2:
-    // 209 -> 199 us; 4 no better); one-lane bf16 neurons and channel-major
-    // neurons over several lanes gained nothing and keep 1.
+    // (3-9 % faster than 1; 4 no better); the channel-major layout likewise (one
+    // lane: 464 -> 435 us; B = 8 over two lanes: 934 -> 872 us, 923 with nw = 2);
+    // bf16 8-byte rows lost 2-6 % (nw = 4 over two lanes: -1.3 %, not kept).
+    // Forward: nw = 4 when a neuron spans several lanes (cifar 411 -> 395 us), 2
+    // for fp32 with one lane per neuron (P = 4 on B = 2: 209 -> 199 us; 4 no
+    // better); one-lane bf16 neurons and channel-major neurons over several
+    // lanes gained nothing and keep 1.
     int nw = 1;
     if (bwd) {
-      if (c->T == 4 && p.BL * p.KC * esz == 16) nw = p.cm ? (L == 1 ? 2 : 1) : (L == 1 ? 2 : 4);
+      if (c->T == 4 && p.BL * p.KC * esz == 16) nw = L == 1 ? 2 : 4;
     } else if (L >= 2) {
       nw = p.cm ? 1 : 4;
     } else if (esz == 4) {
