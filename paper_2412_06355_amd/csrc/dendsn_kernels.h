@@ -645,7 +645,7 @@ __device__ __forceinline__ Pos locate(const ScanArgs& a) {
   const int tid = threadIdx.x;
   r.sub = tid % L;
   const int q = tid / L;
-  // nw > 1 (spatial tiles, backward): each wave covers nw * 64 / L adjacent
+  // nw > 1 (spatial tiles): each wave covers nw * 64 / L adjacent
   // positions, a lane taking slot q of each 64 / L stretch, so each of the nw
   // accesses per row is contiguous across the wave.
   constexpr int kSlots = 64 / L;
@@ -1230,17 +1230,9 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const float beta_r = ba.detach ? 0.0f : a.beta;
-  const int64_t step = int64_t(a.ways) * a.M;  // neurons between this lane's items
-  // A lane visits its nw positions of each item in turn (neurons n, n + 64 / L,
-  // ...), then the next item.  n indexes the [T, N] rows; nx is the matching
-  // element offset of X / grad_x rows (n P, or in the channel-major layout the
-  // item's base plus the position shift).
-  const int nw = a.nw > 1 ? a.nw : 1;
-  const int64_t dn = 64 / L;                              // position shift inside an item
-  const int64_t dnx = kCM<V> ? dn : dn * a.P;
-  const int64_t dn_item = step - (nw - 1) * dn;           // last position -> next item
-  const int64_t dnx_item = step * a.P - (nw - 1) * dnx;
-  const int nvis = nw * nk;
+  // The lane's nw positions of each item in turn, then the next item (Walk).
+  const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
+  const int nvis = wk.nw * nk;
   int64_t n0 = bt0 * a.M, nx0 = bt0 * a.M * a.P;
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
@@ -1269,10 +1261,10 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
     Stash<BL, KS, V> st;
     recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, xin, st);
     if (more) {
-      const bool last_w = ++w == nw;
+      const bool last_w = ++w == wk.nw;
       if (last_w) w = 0;
-      n0 += last_w ? dn_item : dn;
-      nx0 += last_w ? dnx_item : dnx;
+      n0 += last_w ? wk.dn_item : wk.dn;
+      nx0 += last_w ? wk.dnx_item : wk.dnx;
       load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
     }
     reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, in.gv, bl, acc);
