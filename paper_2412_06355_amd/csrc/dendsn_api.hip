@@ -256,11 +256,12 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   }
   // Batch groups (measured on MI355X): the backward wants ~16K waves in the grid
   // (more groups mean more partial sums to reduce; 32K was 1-3 % slower); the
-  // forward over conv layers does best with about four neurons (batch items x
-  // positions) per lane for fp32 and eight for bf16 (4-5 % faster than four).
+  // forward over conv layers does best with one batch item per lane for fp32
+  // (with the XCD eighths below: 1.5-4 % faster than two or four) and eight
+  // neurons (batch items x positions) per lane for bf16 (4-5 % faster than four).
   const int64_t target_waves = 16384;
   int64_t G = ceil_div(target_waves, p.ntiles * 4);
-  if (!bwd && p.mode == kSpatial) G = ceil_div(c->batch * p.nw, esz == 2 ? 8 : 4);
+  if (!bwd && p.mode == kSpatial) G = esz == 2 ? ceil_div(c->batch * p.nw, 8) : c->batch;
   // fully connected tiles (both directions): four batch items per wave (dbg: the
   // same as ~16K waves; long horizon, T = 64: forward -5 %, backward -3 %)
   if (p.mode == kFC) G = ceil_div(c->batch, int64_t(p.ways) * 4);
