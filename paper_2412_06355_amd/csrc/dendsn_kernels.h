@@ -95,36 +95,6 @@ __device__ __forceinline__ void load_vec(const float* __restrict__ p, float (&v)
 }
 
 template <int BL>
-__device__ __forceinline__ void load_vec(const bf16_t* __restrict__ p, float (&v)[BL]) {
-  if constexpr (BL % 8 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 8; ++i) {
-      const u32x4_t q = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p) + i);
-      v[8 * i + 0] = bf16_lo(q.x); v[8 * i + 1] = bf16_hi(q.x);
-      v[8 * i + 2] = bf16_lo(q.y); v[8 * i + 3] = bf16_hi(q.y);
-      v[8 * i + 4] = bf16_lo(q.z); v[8 * i + 5] = bf16_hi(q.z);
-      v[8 * i + 6] = bf16_lo(q.w); v[8 * i + 7] = bf16_hi(q.w);
-    }
-  } else if constexpr (BL % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 4; ++i) {
-      const u32x2_t q = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p) + i);
-      v[4 * i + 0] = bf16_lo(q.x); v[4 * i + 1] = bf16_hi(q.x);
-      v[4 * i + 2] = bf16_lo(q.y); v[4 * i + 3] = bf16_hi(q.y);
-    }
-  } else if constexpr (BL % 2 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 2; ++i) {
-      const uint32_t q = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + i);
-      v[2 * i] = bf16_lo(q); v[2 * i + 1] = bf16_hi(q);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < BL; ++i) v[i] = bf16_lo(__builtin_nontemporal_load(p + i));
-  }
-}
-
-template <int BL>
 __device__ __forceinline__ void store_vec(float* __restrict__ p, const float (&v)[BL]) {
   if constexpr (BL % 4 == 0) {
 #pragma unroll
@@ -139,35 +109,6 @@ __device__ __forceinline__ void store_vec(float* __restrict__ p, const float (&v
   }
 }
 
-template <int BL>
-__device__ __forceinline__ void store_vec(bf16_t* __restrict__ p, const float (&v)[BL]) {
-  if constexpr (BL % 8 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 8; ++i) {
-      uint4 q;
-      q.x = pack_bf16x2(v[8 * i + 0], v[8 * i + 1]);
-      q.y = pack_bf16x2(v[8 * i + 2], v[8 * i + 3]);
-      q.z = pack_bf16x2(v[8 * i + 4], v[8 * i + 5]);
-      q.w = pack_bf16x2(v[8 * i + 6], v[8 * i + 7]);
-      reinterpret_cast<uint4*>(p)[i] = q;
-    }
-  } else if constexpr (BL % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 4; ++i) {
-      uint2 q;
-      q.x = pack_bf16x2(v[4 * i + 0], v[4 * i + 1]);
-      q.y = pack_bf16x2(v[4 * i + 2], v[4 * i + 3]);
-      reinterpret_cast<uint2*>(p)[i] = q;
-    }
-  } else if constexpr (BL % 2 == 0) {
-#pragma unroll
-    for (int i = 0; i < BL / 2; ++i) reinterpret_cast<uint32_t*>(p)[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < BL; ++i) p[i] = to_bf16(v[i]);
-  }
-}
-
 // Address = wave-uniform base (scalar registers) + 32-bit per-lane byte offset.
 template <typename P>
 __device__ __forceinline__ P* at(P* base, uint32_t off) {
@@ -178,8 +119,6 @@ __device__ __forceinline__ const P* at(const P* base, uint32_t off) {
   return reinterpret_cast<const P*>(reinterpret_cast<const char*>(base) + off);
 }
 
-__device__ __forceinline__ float load_one(const float* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ float load_one(const bf16_t* p) { return bf16_lo(__builtin_nontemporal_load(p)); }
 
 // ---------------------------------------------------------------------------
 // Streamed rows through buffer resources: the row base is wave-uniform (scalar
@@ -321,27 +260,15 @@ __device__ __forceinline__ void bstore_one(rsrc_t r, uint32_t off, uint32_t soff
 // (a vector access at the lane offset) or, in the channel-major layout, es
 // bytes apart (one access each, the uniform i * es in the scalar offset; the
 // lanes of a wave hold adjacent positions, so each access is contiguous across
-// the wave).
-// BUF: through a buffer resource (measured faster in the backward, where
-// VALU issue is the co-limiter), else a global access at base + offset
-// (measured faster in the forward).
-template <int E, bool CM, bool BUF, typename IO>
+// the wave).  Through a buffer resource: the backward's segment path.
+template <int E, bool CM, typename IO>
 __device__ __forceinline__ void load_x(const IO* row, uint32_t off, uint32_t es, float (&v)[E]) {
-  if constexpr (!BUF) {
-    if constexpr (CM) {
+  const rsrc_t r = make_rsrc(row);
+  if constexpr (CM) {
 #pragma unroll
-      for (int i = 0; i < E; ++i) v[i] = load_one(at(row, off + uint32_t(i) * es));
-    } else {
-      load_vec<E>(at(row, off), v);
-    }
+    for (int i = 0; i < E; ++i) v[i] = bload_one(r, off, uint32_t(i) * es, row);
   } else {
-    const rsrc_t r = make_rsrc(row);
-    if constexpr (CM) {
-#pragma unroll
-      for (int i = 0; i < E; ++i) v[i] = bload_one(r, off, uint32_t(i) * es, row);
-    } else {
-      bload_vec<E>(r, off, v, row);
-    }
+    bload_vec<E>(r, off, v, row);
   }
 }
 
@@ -941,7 +868,7 @@ __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& 
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
     const int64_t t = c0 + k;
-    load_x<E, CM, true>(xbase + t * rowX, lo.x, a.xes, in.x[k]);
+    load_x<E, CM>(xbase + t * rowX, lo.x, a.xes, in.x[k]);
     in.gs[k] = load_row_one(gsbase + t * a.N, lo.s);
   }
   load_chunk_gv<E, CS>(a, lo, gvbase, c0, in);
@@ -1129,7 +1056,7 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
   const int64_t rowX = a.N * a.P;
   for (int t = t_from; t < t_to; ++t) {
     float xv[E];
-    load_x<E, kCM<V>, true>(xbase + int64_t(t) * rowX, lo.x, a.xes, xv);
+    load_x<E, kCM<V>>(xbase + int64_t(t) * rowX, lo.x, a.xes, xv);
     const float z = dendrite_step<BL, L, V>(vd, xv, br, alpha);
     soma_step(h, s, z, a.beta, a.vth);
   }
