@@ -139,6 +139,18 @@ def test_forward_positions_per_lane(gpu_device, shape, variant):
     compare(case, run_gpu(case, gpu_device))
 
 
+# --- fully connected layers large enough for XCD runs of 32 blocks ---
+@pytest.mark.parametrize("shape", [(8, 32, 2048, 16, "f32", 4), (4, 64, 1024, 32, "f32", 4),
+                                   (6, 32, 8192, 8, "bf16", 3)],
+                         ids=lambda s: "T{}b{}C{}B{}{}K{}".format(*s))
+def test_fully_connected_xcd_runs(gpu_device, shape):
+    T, batch, C, B, io, K = shape
+    c = cfg(T=T, batch=batch, C=C, S=1, B=B, io=io, ckpt_every=K, beta=0.7)
+    seed = zlib.crc32(repr((shape, "fc-xcd")).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.6, mask_rho=0.5, name=f"fc-xcd/{shape}", with_gv=True)
+    compare(case, run_gpu(case, gpu_device))
+
+
 # --- several compartments per branch (L2 norm over a branch's compartments) ---
 KC_SHAPES = [
     # T, batch, C, S, B, k, io, K
