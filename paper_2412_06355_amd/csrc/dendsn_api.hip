@@ -105,14 +105,15 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 // (BL, L) for KC compartments per branch.  KC = 1: a vector-width lane split
 // when the branch count allows one (16 bytes per lane; the bf16 backward takes
-// 8 bytes, 4 branches, per lane up to 64 branches: measured 10 % faster than 8
-// branches per lane, whose stash spills), else a generic split with up to 8
-// branches per lane over 1 or 2 lanes.  KC = 2 or 4: 16 bytes of compartments per lane
+// 8 bytes, 4 branches, per lane from 16 up to 64 branches: measured 10 % faster
+// than 8 branches per lane, whose stash fills the registers; with 8 branches
+// one lane of 8 is 3 % faster than two lanes of 4, half the soma work per
+// branch), else a generic split with up to 8 branches per lane over 1 or 2 lanes.  KC = 2 or 4: 16 bytes of compartments per lane
 // (BL KC = 4 for fp32, 8 for bf16) when the branch count allows, else one lane
 // holds the whole neuron (B KC <= 14).
 bool choose_mapping(int B, int KC, int io, bool bwd, int* BL, int* L, int* fast) {
   if (KC == 1) {
-    const int blv = (io == DENDSN_IO_BF16 && B % 8 == 0 && !(bwd && B <= 64)) ? 8 : 4;
+    const int blv = (io == DENDSN_IO_BF16 && B % 8 == 0 && !(bwd && B > 8 && B <= 64)) ? 8 : 4;
     if (B % blv == 0 && is_pow2(B / blv) && B / blv <= 16) {
       *BL = blv; *L = B / blv; *fast = 1;
       return true;
