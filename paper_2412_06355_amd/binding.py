@@ -125,7 +125,7 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
                 f"{LIB_PATH} is missing: build the HIP library first "
-                "(python -c 'import __graft_entry__ as g; g.build()')")
+                "(python -m paper_2412_06355_amd.build)")
         handle = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGS.items():
             fn = getattr(handle, name)
