@@ -130,8 +130,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the DendSN scan is "
-              "not sharded across GPUs in this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library runs the "
+              "DendSN scan on a single GPU.", file=sys.stderr)
         sys.exit(2)
 
     import torch

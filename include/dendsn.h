@@ -75,7 +75,7 @@ extern "C" {
 typedef enum dendsn_status {
     DENDSN_OK = 0,
     DENDSN_E_INVALID = 1,      /* an argument violates the contract            */
-    DENDSN_E_UNSUPPORTED = 2,  /* valid model, but a shape this build rejects   */
+    DENDSN_E_UNSUPPORTED = 2,  /* valid model, but a shape no compiled kernel covers */
     DENDSN_E_WORKSPACE = 3,    /* workspace missing or smaller than required    */
     DENDSN_E_HIP = 4           /* a kernel launch failed                        */
 } dendsn_status;

@@ -191,10 +191,10 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
   int BL, L, fast;
   if (channel_major(c)) {
     if (!cm_mapping(c->B, c->comps_per_branch, &BL, &L))
-      return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build in the channel-major layout");
+      return fail(DENDSN_E_UNSUPPORTED, "branch count not covered by the compiled channel-major kernels");
   } else if (!choose_mapping(c->B, c->comps_per_branch, c->io, false, &BL, &L, &fast) ||
              !choose_mapping(c->B, c->comps_per_branch, c->io, true, &BL, &L, &fast)) {
-    return fail(DENDSN_E_UNSUPPORTED, "branch count not supported by this build");
+    return fail(DENDSN_E_UNSUPPORTED, "branch count not covered by the compiled kernels");
   }
   return DENDSN_OK;
 }
