@@ -120,7 +120,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=30)  # the clocks ramp over the first ~30 ms of work
     ap.add_argument("--workload", default="cifar")
     ap.add_argument("--batch-groups", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
