@@ -32,13 +32,14 @@ hipError_t launch_bwd_bf16_cm_sg1(const Plan& pl, const BwdArgs& ba, int v, hipS
 // Fixed-order float64 sums of the per-block partials into the parameter
 // gradients.  Outputs o = c * W + ol with W = 2 B + P: ol < B is g_kappa of
 // branch ol, then g_xi of the P compartments, then g_zeta of the B branches.
-// The last block reduces the g_alpha partials, the one before g_beta's.
+// Blocks 0 and 1 reduce the g_alpha and g_beta partials (first, so that their
+// longer serial sums overlap the rest).
 __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   const int tid = threadIdx.x;
   const int W = 2 * f.B + f.P;
   const int64_t nout = f.C * W;
-  if (blockIdx.x >= gridDim.x - 2) {  // last block: g_alpha; the one before: g_beta
-    const bool is_alpha = blockIdx.x == gridDim.x - 1;
+  if (blockIdx.x < 2) {  // block 0: g_alpha; block 1: g_beta
+    const bool is_alpha = blockIdx.x == 0;
     const float* src = is_alpha ? f.wsA : f.wsB;
     __shared__ double sh[kThreads];
     double s = 0.0;
@@ -58,14 +59,14 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   int64_t o;
   double s = 0.0;
   if (f.wide) {  // one wave per output, lanes stride over its contiguous slots
-    o = int64_t(blockIdx.x) * (kThreads / 64) + (tid >> 6);
+    o = int64_t(blockIdx.x - 2) * (kThreads / 64) + (tid >> 6);
     const int lane = tid & 63;
     if (o < nout)
       for (int64_t p = lane; p < f.slots; p += 64) s += double(f.wsP[o * f.slots + p]);
     for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
     if (lane != 0 || o >= nout) return;
   } else {       // one thread per output, slots in order
-    o = int64_t(blockIdx.x) * kThreads + tid;
+    o = int64_t(blockIdx.x - 2) * kThreads + tid;
     if (o >= nout) return;
     for (int64_t p = 0; p < f.slots; ++p) s += double(f.wsP[p * nout + o]);
   }

@@ -1356,8 +1356,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
   reduce_partials<BL, E, L>(ba, pos, acc);
 }
 
-// Fixed-order float64 sum of the partials into the parameter gradients; the
-// last block reduces g_alpha.
+// Fixed-order float64 sum of the partials into the parameter gradients;
+// blocks 0 and 1 reduce g_alpha and g_beta.
 __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f);
 
 }  // namespace dendsn
