@@ -464,17 +464,42 @@ template <int BL, int KC>
 __device__ __forceinline__ void load_branches(const ScanArgs& a, int64_t c, int sub, Branches<BL, KC>& br,
                                               bool packed_pairs = false) {
   const int64_t base = c * a.B + int64_t(sub) * BL;
+  const int64_t base_i = c * a.P + int64_t(sub) * (BL * KC);
+  // Every load is issued before any value is used (the null checks are uniform
+  // branches around whole groups), so the lot costs one memory round trip.
+  float kap[BL], zet[BL];
+  uint32_t msk[BL];
+#pragma unroll
+  for (int j = 0; j < BL; ++j) kap[j] = a.kappa[base + j];
+  if (a.zeta) {
+#pragma unroll
+    for (int j = 0; j < BL; ++j) zet[j] = a.zeta[base + j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < BL; ++j) zet[j] = 1.0f;
+  }
+  if (a.mask) {
+#pragma unroll
+    for (int j = 0; j < BL; ++j) msk[j] = a.mask[base + j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < BL; ++j) msk[j] = 1;
+  }
+  if (a.xi) {
+#pragma unroll
+    for (int i = 0; i < BL * KC; ++i) br.xi[i] = a.xi[base_i + i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < BL * KC; ++i) br.xi[i] = 0.0f;
+  }
 #pragma unroll
   for (int j = 0; j < BL; ++j) {
-    const bool on = a.mask ? (a.mask[base + j] != 0) : true;
+    const bool on = msk[j] != 0;
     br.on[j] = on;
-    br.k[j] = on ? a.kappa[base + j] : 0.0f;
-    br.rz[j] = a.zeta ? 1.0f / a.zeta[base + j] : 1.0f;
+    br.k[j] = on ? kap[j] : 0.0f;
+    br.rz[j] = 1.0f / zet[j];
     br.krz[j] = br.k[j] * br.rz[j];
   }
-  const int64_t base_i = c * a.P + int64_t(sub) * (BL * KC);
-#pragma unroll
-  for (int i = 0; i < BL * KC; ++i) br.xi[i] = a.xi ? a.xi[base_i + i] : 0.0f;
   br.rp = a.rP;
 #pragma unroll
   for (int i = 0; i < BL * KC; ++i)
