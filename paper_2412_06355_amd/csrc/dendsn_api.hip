@@ -42,8 +42,20 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
     const bool is_alpha = blockIdx.x == 0;
     const float* src = is_alpha ? f.wsA : f.wsB;
     __shared__ double sh[kThreads];
+    // A thread sums src[tid], src[tid + 256], ... in that order.  Eight loads
+    // are issued together, unconditionally (an index past the end reads the
+    // last element again and its term is dropped), so they share one round trip.
+    constexpr int U = 8;
+    const int64_t last = f.nA - 1;
     double s = 0.0;
-    for (int64_t i = tid; i < f.nA; i += kThreads) s += double(src[i]);
+    for (int64_t i0 = tid; i0 < f.nA; i0 += int64_t(U) * kThreads) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = src[min(i0 + int64_t(u) * kThreads, last)];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + int64_t(u) * kThreads <= last) s += double(v[u]);
+    }
     sh[tid] = s;
     __syncthreads();
     for (int w = kThreads / 2; w >= 1; w >>= 1) {
@@ -56,22 +68,16 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
     }
     return;
   }
-  int64_t o;
-  double s = 0.0;
-  if (f.wide) {  // one wave per output, lanes stride over its contiguous slots
-    o = int64_t(blockIdx.x - 2) * (kThreads / 64) + (tid >> 6);
-    const int lane = tid & 63;
-    if (o < nout)
-      for (int64_t p = lane; p < f.slots; p += 64) s += double(f.wsP[o * f.slots + p]);
-    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-    if (lane != 0 || o >= nout) return;
-  } else {       // one thread per output, slots in order
-    o = int64_t(blockIdx.x - 2) * kThreads + tid;
-    if (o >= nout) return;
-    for (int64_t p = 0; p < f.slots; ++p) s += double(f.wsP[p * nout + o]);
-  }
-  const int64_t c = o / W;
-  const int ol = int(o % W);
+  const bool wide = f.wide != 0;
+  const int lane = tid & 63;
+  const int64_t o = wide ? int64_t(blockIdx.x - 2) * (kThreads / 64) + (tid >> 6)
+                         : int64_t(blockIdx.x - 2) * kThreads + tid;
+  if (!wide && o >= nout) return;  // (wide: every lane stays for the shuffles)
+  // Where the output goes, worked out first so that its branch's gate is read
+  // in the same round trip as the partial sums.
+  const int64_t oq = o < nout ? o : nout - 1;
+  const int64_t c = oq / W;
+  const int ol = int(oq % W);
   float* out;
   int64_t idx;
   int b;  // the branch the output belongs to
@@ -82,8 +88,31 @@ __global__ void __launch_bounds__(kThreads) dendsn_finalize_kernel(FinArgs f) {
   } else {
     out = f.gz; idx = c * f.B + (ol - f.B - f.P); b = ol - f.B - f.P;
   }
+  const uint8_t* gate = f.mask ? f.mask + c * f.B + b : nullptr;
+  bool on = true;
+  double s = 0.0;
+  if (wide) {  // one wave per output, lanes stride over its contiguous slots
+    if (o < nout)
+      for (int64_t p = lane; p < f.slots; p += 64) s += double(f.wsP[o * f.slots + p]);
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (lane != 0 || o >= nout) return;
+    if (gate) on = *gate != 0;
+  } else {     // one thread per output, slots in order
+    // slots in groups of four, each group's loads issued together (a slot past
+    // the last reads the last one again and its term is dropped); the gate is
+    // read behind the first group's loads
+    const int64_t last = f.slots - 1;
+    for (int64_t p0 = 0; p0 <= last; p0 += 4) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = f.wsP[min(p0 + u, last) * nout + o];
+      if (p0 == 0 && gate) on = *gate != 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (p0 + u <= last) s += double(v[u]);
+    }
+  }
   if (!out) return;
-  const bool on = f.mask ? (f.mask[c * f.B + b] != 0) : true;
   out[idx] = on ? float(s) : 0.0f;
 }
 
