@@ -702,8 +702,11 @@ __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, 
                                            uint32_t (&buf)[D][kRawW<IO, BL, CM>]) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
-    const int t = min(cur.t + k, T - 1);
-    load_raw<IO, BL, CM>(cur.base + int64_t(t) * rowX, ox, a.xes, buf[k]);
+    // A padding step past T (its result is discarded): every lane reads the
+    // start of row T - 1, one cache line per wave instead of a whole row.
+    const int tk = cur.t + k;
+    const int t = min(tk, T - 1);
+    load_raw<IO, BL, CM>(cur.base + int64_t(t) * rowX, tk < T ? ox : 0u, a.xes, buf[k]);
   }
   cur.t += D;
   if (cur.t >= Tp) {
