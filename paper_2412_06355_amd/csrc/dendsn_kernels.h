@@ -197,49 +197,49 @@ __device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL]
   }
 }
 
-template <int BL>
+template <int BL, int AUX = kAuxNT>
 __device__ __forceinline__ void bstore_vec(rsrc_t r, uint32_t off, const float (&v)[BL], float*) {
   if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
       const u32x4_t q = {__float_as_uint(v[4 * i]), __float_as_uint(v[4 * i + 1]), __float_as_uint(v[4 * i + 2]),
                          __float_as_uint(v[4 * i + 3])};
-      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, kAuxNT);
+      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, AUX);
     }
   } else if constexpr (BL % 2 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 2; ++i) {
       const u32x2_t q = {__float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1])};
-      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, kAuxNT);
+      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, AUX);
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), r, off + 4u * i, 0, kAuxNT);
+    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), r, off + 4u * i, 0, AUX);
   }
 }
 
-template <int BL>
+template <int BL, int AUX = kAuxNT>
 __device__ __forceinline__ void bstore_vec(rsrc_t r, uint32_t off, const float (&v)[BL], bf16_t*) {
   if constexpr (BL % 8 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 8; ++i) {
       const u32x4_t q = {pack_bf16x2(v[8 * i + 0], v[8 * i + 1]), pack_bf16x2(v[8 * i + 2], v[8 * i + 3]),
                          pack_bf16x2(v[8 * i + 4], v[8 * i + 5]), pack_bf16x2(v[8 * i + 6], v[8 * i + 7])};
-      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, kAuxNT);
+      __builtin_amdgcn_raw_buffer_store_b128(q, r, off + 16u * i, 0, AUX);
     }
   } else if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
       const u32x2_t q = {pack_bf16x2(v[4 * i + 0], v[4 * i + 1]), pack_bf16x2(v[4 * i + 2], v[4 * i + 3])};
-      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, kAuxNT);
+      __builtin_amdgcn_raw_buffer_store_b64(q, r, off + 8u * i, 0, AUX);
     }
   } else if constexpr (BL % 2 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 2; ++i)
-      __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(v[2 * i], v[2 * i + 1]), r, off + 4u * i, 0, kAuxNT);
+      __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(v[2 * i], v[2 * i + 1]), r, off + 4u * i, 0, AUX);
   } else {
 #pragma unroll
-    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v[i]), r, off + 2u * i, 0, kAuxNT);
+    for (int i = 0; i < BL; ++i) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v[i]), r, off + 2u * i, 0, AUX);
   }
 }
 
@@ -279,7 +279,13 @@ __device__ __forceinline__ void store_gx(IO* row, uint32_t off, uint32_t es, con
 #pragma unroll
     for (int i = 0; i < E; ++i) bstore_one(r, off, uint32_t(i) * es, v[i], row);
   } else {
-    bstore_vec<E>(r, off, v, row);
+    // Non-temporal up to 16 bytes a lane.  A longer row is several stores, each
+    // writing every line it touches in pieces; as streaming stores the pieces
+    // reached HBM separately (the ten-compartment fp32 rows wrote 32 % more
+    // than grad_x, 1 % slower), so those go through L2 as default stores.
+    // (Shorter multi-store rows, e.g. 12-byte bf16 ones, ran 1.7 % slower so.)
+    constexpr bool streaming = E * sizeof(IO) <= 16;
+    bstore_vec<E, streaming ? kAuxNT : 0>(r, off, v, row);
   }
 }
 
