@@ -26,7 +26,17 @@ def _dump(t, path):
     return (str(path), list(a.shape))
 
 
-@pytest.mark.parametrize("name", ["cifar", "imagenet_stem", "long_horizon", "dbg"])
+def _npb(t, wl):
+    """X or grad_x in the oracle's [T, N, P] order: a channel-major tensor's memory
+    is [T, batch, C, P, S], its compartments S elements apart."""
+    if wl.layout != "channel_major":
+        return t
+    return t.reshape(wl.T, wl.batch, wl.C, wl.P, wl.S).permute(0, 1, 2, 4, 3).reshape(wl.T, wl.N, wl.P)
+
+
+# every benchmark layer (bench.py --workload W), in the launch configuration it times
+@pytest.mark.parametrize("name", ["cifar", "imagenet_stem", "long_horizon", "dbg", "cifar_bf16", "cifar_p4b2",
+                                  "cifar_p4b2_cm", "cifar_cm", "tiny_imagenet_res", "dvs_p10b5"])
 def test_full_size_against_oracle(gpu_device, name, tmp_path):
     import torch
 
@@ -46,9 +56,9 @@ def test_full_size_against_oracle(gpu_device, name, tmp_path):
     g = dendsn.backward(cfg, X, alpha, kappa, None, None, mask, ckpt, gS)
     torch.cuda.synchronize(gpu_device)
 
-    files = dict(X=_dump(X, tmp_path / "X.f32"), gS=_dump(gS, tmp_path / "gS.f32"),
+    files = dict(X=_dump(_npb(X, wl), tmp_path / "X.f32"), gS=_dump(gS, tmp_path / "gS.f32"),
                  S=_dump(spikes, tmp_path / "S.f32"), H=_dump(v_soma, tmp_path / "H.f32"),
-                 gX=_dump(g["grad_x"], tmp_path / "gX.f32"))
+                 gX=_dump(_npb(g["grad_x"], wl), tmp_path / "gX.f32"))
     grads = {k: g[k].cpu().numpy().astype(np.float64) for k in ("grad_kappa", "grad_xi", "grad_zeta")}
     g_alpha, g_beta = float(g["grad_alpha"].item()), float(g["grad_beta"].item())
     del X, gS, spikes, v_soma, ckpt, g
