@@ -227,3 +227,18 @@ def test_product_code_never_touches_the_oracle():
                 text = open(os.path.join(base, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "dendsn_oracle" not in text, f
+
+
+def test_sample_slice_limit(lib):
+    # Lane offsets inside one sample's [C, S, P] slice are 32-bit byte offsets:
+    # 255 channels of 2^20 positions x 4 fp32 branches (4,278,190,080 bytes) are
+    # the largest slice tests run on the GPU; one more channel (exactly 4 GiB) is
+    # refused before any launch, in both directions.
+    cfg = base_cfg(T=2, batch=2, C=256, S=1 << 20, B=4, ckpt_every=1)
+    assert fwd(lib, cfg, ckpt=GOOD + 0x800) == E_UNSUPPORTED
+    assert "4 GiB" in dendsn.dendsn_last_error()
+    assert bwd(lib, cfg, ckpt=GOOD + 0x800) == E_UNSUPPORTED
+    out = ctypes.c_size_t(0)
+    ok = base_cfg(T=2, batch=2, C=255, S=1 << 20, B=4, ckpt_every=1)
+    assert lib.dendsn_ckpt_bytes(ctypes.byref(ok), ctypes.byref(out)) == 0
+    assert out.value == 2 * 255 * (1 << 20) * 5 * 4   # one checkpoint: N (P + 1) floats, N = 2 C S
