@@ -56,6 +56,14 @@
  *     first failed check is available from dendsn_last_error() on the calling
  *     thread.  A failed launch returns DENDSN_E_HIP.  Faults inside a kernel
  *     surface at the caller's next synchronisation.
+ *   - An empty layer (T, batch, C or S of 0) is refused with DENDSN_E_INVALID:
+ *     there is nothing to compute and no gradient to define, so the caller skips
+ *     the call.
+ *   - Size limits, refused with DENDSN_E_UNSUPPORTED: one sample's slice of X
+ *     (C * S * P elements) must stay below 4 GiB, since lanes address it with
+ *     32-bit byte offsets (whole tensors may be larger); the grid must stay below
+ *     2^31 blocks.  Counts beyond 2^46 elements (N, or T * N * P) are refused
+ *     with DENDSN_E_INVALID.
  *   - Not checked (it would need a device synchronisation): zeta > 0,
  *     0 <= alpha < 1, finite inputs, and that pointers address device memory of
  *     the stated size.
