@@ -474,3 +474,55 @@ def test_forward_without_checkpoints_for_inference(gpu_device):
     torch.cuda.synchronize()
     assert ck is not None and ck2 is None
     assert torch.equal(s1, s2) and torch.equal(v1, v2)
+
+
+# --- degenerate cases of the method ---
+def _degenerate(name, io):
+    """A seeded case in one of the method's degenerate regimes."""
+    stateless = name.startswith("x-equals-xi")
+    kc = 2 if name.endswith("kc2") else 1
+    c = cfg(T=5, batch=2, C=16, S=300, B=4, io=io, comps_per_branch=kc, ckpt_every=2,
+            stateful=not stateless, residual=name == "all-gated-res",
+            psi="identity" if name.endswith("id-kc2") else "mexhat",
+            beta=0.0 if name == "beta-zero" else 0.5,
+            v_th=0.0 if name == "always-fire" else 1.0)
+    # saturated: X ~ N(1000, 10) keeps u >= 500, where exp(-u^2/2) underflows to 0 in fp32 and
+    # fp64 alike (a zero-mean spread of 1000 would instead test fp32 cancellation in Vd)
+    sat = name == "saturated"
+    case = make_case(c, seed=zlib.crc32(f"{name}/{io}".encode()) % 1000, x_mean=1000.0 if sat else 0.0,
+                     x_std=10.0 if sat else 1.2,
+                     alpha=0.6, random_affine=True, mask_rho=0.5, name=f"degenerate/{name}/{io}")
+    if name.startswith("all-gated"):
+        case.mask = np.zeros_like(case.mask)             # every branch of every channel gated off
+    else:
+        case.mask = None
+    if name in ("kappa-zero", "always-fire"):
+        case.kappa = np.zeros_like(case.kappa)            # Z = 0: H stays 0 (always at threshold when v_th = 0)
+    if stateless:
+        # Vd = X = xi exactly: every branch at the norm's origin (zero subgradient)
+        cidx = (np.arange(c.N) // c.S) % c.C
+        case.X = np.broadcast_to(case.xi[cidx][None], case.X.shape).copy()
+        if io == "bf16":
+            import torch
+
+            case.xi = torch.from_numpy(case.xi).to(torch.bfloat16).float().numpy()
+            case.X = np.broadcast_to(case.xi[cidx][None], case.X.shape).copy()
+    return case
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("name", ["all-gated", "all-gated-res", "kappa-zero", "always-fire", "beta-zero",
+                                  "x-equals-xi", "x-equals-xi-id-kc2", "saturated"])
+def test_degenerate_cases(gpu_device, name, io):
+    case = _degenerate(name, io)
+    gpu = run_gpu(case, gpu_device)
+    rep = compare(case, gpu)
+    if name in ("kappa-zero", "always-fire") or name == "all-gated":
+        assert np.all(gpu["gX"] == 0.0)                   # nothing reaches X's gradient but through Z
+    if name == "always-fire":
+        assert np.all(gpu["S"] == 1.0)                    # H = 0 = v_th fires (Theta(0) = 1) at every step
+    if name.startswith("x-equals-xi"):
+        assert np.all(gpu["gX"] == 0.0)                   # the norm's subgradient at 0 is 0
+    if name == "saturated":                               # psi = psi' = 0 on every branch: a silent layer
+        assert np.all(gpu["S"] == 0.0) and np.all(gpu["H"] == 0.0) and np.all(gpu["gX"] == 0.0)
+    print(name, io, rep)
