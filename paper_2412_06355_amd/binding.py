@@ -241,6 +241,24 @@ def _check_params(cfg, x, alpha, kappa, xi, zeta, mask, beta=None):
     _expect(mask, "mask", (cfg.C, cfg.B), torch.uint8, dev, optional=True)
 
 
+def _check_ckpt(cfg, ckpt, device):
+    """The checkpoint buffer the backward reads: when this cfg has interior
+    checkpoints, a contiguous float32 tensor on the layer's device holding at
+    least dendsn_ckpt_bytes(cfg) bytes (a buffer written for another cfg would
+    be read past its end)."""
+    import torch
+
+    need = dendsn_ckpt_bytes(cfg)
+    if need == 0:
+        return
+    if ckpt is None:
+        raise ValueError(f"ckpt is required: this layer has interior checkpoints ({need} bytes)")
+    if ckpt.dtype != torch.float32 or ckpt.device != device or not ckpt.is_contiguous():
+        raise ValueError(f"ckpt must be a contiguous float32 tensor on {device}")
+    if ckpt.numel() * 4 < need:
+        raise ValueError(f"ckpt holds {ckpt.numel() * 4} bytes, this layer needs {need}")
+
+
 def forward(cfg: DendSNConfig, x, alpha, kappa, xi=None, zeta=None, mask=None, *, beta=None,
             want_v_soma: bool = False, save_ckpt: bool = True):
     """Returns (spikes [T,N] io, v_soma [T,N] fp32 or None, ckpt buffer or None).
@@ -267,6 +285,7 @@ def backward(cfg: DendSNConfig, x, alpha, kappa, xi, zeta, mask, ckpt, grad_spik
     dev = x.device
     _expect(grad_spikes, "grad_spikes", (cfg.T, cfg.N), _io_dtype(cfg), dev)
     _expect(grad_v_soma, "grad_v_soma", (cfg.T, cfg.N), torch.float32, dev, optional=True)
+    _check_ckpt(cfg, ckpt, dev)
     out = dict(
         grad_x=torch.empty(x.shape, dtype=_io_dtype(cfg), device=dev),
         grad_alpha=torch.empty((1,), dtype=torch.float32, device=dev),

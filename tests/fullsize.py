@@ -9,7 +9,8 @@ from __future__ import annotations
 import numpy as np
 
 import oracle
-from tests.parity import BAND, RTOL_BF16, RTOL_F32
+from tests import fp32_eval
+from tests.parity import BAND, RTOL_F32, tolerance
 
 
 def _open(spec):
@@ -50,25 +51,30 @@ def check_item(job: dict) -> dict:
     else:
         return dict(item=b, error=f"item {b}: forced-spike protocol did not converge")
     g = oracle.backward(rec, gS, sg_kind=p["sg"], sg_scale=p["sg_scale"], detach_reset=p["detach"])
+    # a plain float32 evaluation of the same equations on this item's inputs and
+    # spike train: what float32 arithmetic itself needs here (tests/parity.py)
+    r32 = fp32_eval.evaluate(X, rec["S"], gS, alpha=p["alpha"], beta=p["beta"], v_th=p["v_th"], kappa=p["kappa"],
+                             xi=p["xi"], zeta=p["zeta"], mask=p["mask"], C=p["C"], S=p["S"], psi=p["psi"],
+                             stateful=p["stateful"], residual=p["residual"], k=p["k"], sg=p["sg"],
+                             sg_scale=p["sg_scale"], detach=p["detach"])
     out = dict(item=b, error=None, exempt=exempt)
     # elementwise comparisons of this item's outputs (scale: |o| + rms over the item)
-    for name, got, ref, rtol in (("v_soma", H_g, rec["H"], RTOL_F32 * job["growth"]),
-                                 ("grad_x", gX_g, g["gX"], job["rtol_io"] * job["growth"])):
+    for name, got, ref, f32, rtol in (("v_soma", H_g, rec["H"], r32["H"], RTOL_F32),
+                                      ("grad_x", gX_g, g["gX"], r32["gX"], job["rtol_io"])):
         scale = np.abs(ref) + np.sqrt(np.mean(ref * ref))
         ratio = float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-300)))
+        tol = tolerance(rtol, fp32_eval.elementwise_ratio(f32, ref))
         out["max_" + name] = ratio
-        if ratio > rtol:
-            out["error"] = f"item {b}: {name} error/scale {ratio:.3e} > {rtol:.3g}"
+        if ratio > tol:
+            out["error"] = f"item {b}: {name} error/scale {ratio:.3e} > {tol:.3g}"
             return out
         den = np.linalg.norm(ref)
         nrel = float(np.linalg.norm(got - ref) / den) if den > 0 else 0.0
         if nrel > (RTOL_F32 if name == "v_soma" else job["rtol_io"]):
             out["error"] = f"item {b}: {name} norm-wise error {nrel:.3e}"
             return out
-    for k in ("kappa", "xi", "zeta"):
+    for k in ("kappa", "xi", "zeta", "alpha", "beta"):
         out["g_" + k] = g["g_" + k]
         out["abs_" + k] = g["abs_" + k]
-    for k in ("alpha", "beta"):
-        out["g_" + k] = g["g_" + k]
-        out["abs_" + k] = g["abs_" + k]
+        out["f32_" + k] = r32["g_" + k]      # this item's float32 sums
     return out

@@ -9,24 +9,23 @@ kernel's decision imposed at that step (the oracle then follows the same spike
 train), repeating until no disagreement is left; every exemption is counted and
 reported.  A disagreement outside the band fails.
 
-Tolerances.  fp32 outputs: |g - o| <= rtol (|o| + rms(o)) elementwise, rms over
-the tensor; summed parameter gradients: |g - o| <= rtol (A + rms(A)) with
+Tolerances.  fp32 outputs: |g - o| <= tol (|o| + rms(o)) elementwise, rms over
+the tensor; summed parameter gradients: |g - o| <= tol (A + rms(A)) with
 A = sum|terms| per entry and rms over the [C, B] table (a term of psi = MH can
 vanish by cancellation, (1 - u^2) near u = 1, while its rounding error does not,
-so an entry's own A alone can undercount its rounding); the scalar g_alpha:
-|g - o| <= rtol * A.
-rtol is 1e-5 for fp32 results and 2e-2 for results stored in bf16.  Every
-tensor must also meet ||g - o||_2 <= rtol ||o||_2.
+so an entry's own A alone can undercount its rounding); the scalar g_alpha and
+g_beta: |g - o| <= tol * A.  Every tensor must also meet
+||g - o||_2 <= rtol ||o||_2 with the plain rtol.
 
-Long horizons.  Rounding errors of an fp32 evaluation of the leaky recurrences
-accumulate over the memory of each chain, h(x) = min(T, 1 / (1 - x)) steps for
-a decay x; the somatic potential inherits the dendrite's error (h(alpha)) and
-carries it through the soma (h(beta)), and the backward's surrogate derivative
-is steepest exactly where that potential sits.  The elementwise bounds are
-therefore scaled by g = max(1, h(beta) h(alpha) / 4), which is 1 for four-step
-layers with alpha = beta = 1/2 and 12.5 for T = 64, alpha = 0.8, beta = 0.9 (a
-plain float32 evaluation of the equations on the CPU reaches 3.0e-5 there).
-The norm-wise bound is never scaled.
+tol = max(rtol, FP32_MARGIN * e32): rtol is 1e-5 for fp32 results and 2e-2 for
+results stored in bf16, and e32 is the error, in the same measure, of a plain
+float32 evaluation of the same equations on the same inputs and spike train
+(tests/fp32_eval.py).  On most layers e32 is far below rtol and tol = rtol.
+Long horizons are where it is not: rounding errors of the leaky recurrences
+accumulate over each chain's memory, and the surrogate derivative is steepest
+exactly where the potential sits near threshold (float32 reaches 2.7e-5 on
+grad_x of the T = 64, alpha = 0.8, beta = 0.9 layer), so the bound there is
+1.5 times what float32 itself needs on that input, and never looser.
 """
 
 from __future__ import annotations
@@ -41,6 +40,7 @@ import oracle
 BAND = 1e-6
 RTOL_F32 = 1e-5
 RTOL_BF16 = 2e-2
+FP32_MARGIN = 1.5   # a kernel may be this much less accurate than a plain float32 evaluation
 
 
 def announce(msg: str):
@@ -74,10 +74,12 @@ class Case:
 class Report:
     exemptions: int = 0
     max_err: dict = field(default_factory=dict)
+    fp32: dict = field(default_factory=dict)   # the plain float32 evaluation's errors
 
     def __str__(self):
         errs = ", ".join(f"{k}={v:.2e}" for k, v in self.max_err.items())
-        return f"exemptions={self.exemptions} {errs}"
+        f32 = ", ".join(f"{k}={v:.2e}" for k, v in self.fp32.items())
+        return f"exemptions={self.exemptions} {errs} | float32 evaluation: {f32}"
 
 
 def make_case(cfg, seed=0, x_mean=0.0, x_std=1.0, alpha=0.5, random_affine=True, mask_rho=None,
@@ -208,11 +210,31 @@ def cfg_vth(case):
     return case.cfg.v_th
 
 
-def horizon_growth(cfg, alpha: float, beta: float | None = None) -> float:
-    """Elementwise tolerance factor g = max(1, h(beta) h(alpha) / 4)."""
-    h = lambda x: min(float(cfg.T), 1.0 / (1.0 - x))
-    b = cfg.beta if beta is None else beta
-    return max(1.0, h(b) * (h(alpha) if cfg.stateful else 1.0) / 4.0)
+def fp32_errors(case: Case, rec, og) -> dict:
+    """Errors of a plain float32 evaluation of the equations (tests/fp32_eval.py)
+    against the oracle on this case's inputs and spike train, in the parity
+    measures: elementwise for v_soma and grad_x, summed for the parameter
+    gradients."""
+    from tests import fp32_eval
+
+    cfg = case.cfg
+    r = fp32_eval.evaluate(case.X, rec["S"], case.gS, case.gV, alpha=case.alpha, beta=case.beta, v_th=cfg.v_th,
+                           kappa=case.kappa, xi=case.xi, zeta=case.zeta, mask=case.mask, C=cfg.C, S=cfg.S,
+                           psi=cfg.psi, stateful=cfg.stateful, residual=cfg.residual, k=cfg.comps_per_branch,
+                           sg=cfg.sg, sg_scale=cfg.sg_scale, detach=cfg.detach_reset)
+    e = dict(v_soma=fp32_eval.elementwise_ratio(r["H"], rec["H"]),
+             grad_x=fp32_eval.elementwise_ratio(r["gX"], og["gX"]))
+    for k in ("g_kappa", "g_xi", "g_zeta"):
+        e[k] = fp32_eval.summed_ratio(r[k], og[k], og["abs_" + k[2:]])
+    ok_a = cfg.stateful and og["abs_alpha"] > 0
+    e["g_alpha"] = abs(r["g_alpha"] - og["g_alpha"]) / og["abs_alpha"] if ok_a else 0.0
+    e["g_beta"] = abs(r["g_beta"] - og["g_beta"]) / og["abs_beta"] if og["abs_beta"] > 0 else 0.0
+    return e
+
+
+def tolerance(rtol: float, e32: float) -> float:
+    """The bound of one tensor: rtol, or FP32_MARGIN times what float32 needs."""
+    return max(rtol, FP32_MARGIN * e32)
 
 
 def close_normwise(name, g, o, rtol, report: Report):
@@ -224,20 +246,20 @@ def close_normwise(name, g, o, rtol, report: Report):
         raise AssertionError(f"{name}: norm-wise relative error {rel:.3e} > {rtol:g}")
 
 
-def close_elementwise(name, g, o, rtol, growth, report: Report):
+def close_elementwise(name, g, o, rtol, tol, report: Report):
     close_normwise(name, g, o, rtol, report)
     scale = np.abs(o) + np.sqrt(np.mean(o * o)) if o.size else np.abs(o)
     err = np.abs(g - o)
     ratio = float(np.max(err / np.maximum(scale, 1e-300))) if o.size else 0.0
     report.max_err[name] = ratio
-    bound = rtol * growth * scale
+    bound = tol * scale
     if not np.all(err <= bound):
         i = np.unravel_index(np.argmax(err - bound), o.shape)
         raise AssertionError(f"{name}: |gpu - oracle| too large at {i}: gpu={g[i]!r} oracle={o[i]!r} "
-                             f"(max err/scale {ratio:.3e}, allowed {rtol * growth:.3g})")
+                             f"(max err/scale {ratio:.3e}, allowed {tol:.3g})")
 
 
-def close_summed(name, g, o, absum, rtol, growth, report: Report):
+def close_summed(name, g, o, absum, rtol, tol, report: Report):
     g, o, absum = np.asarray(g, np.float64), np.asarray(o, np.float64), np.asarray(absum, np.float64)
     if np.ndim(o):
         close_normwise(name, g, o, rtol, report)
@@ -245,11 +267,11 @@ def close_summed(name, g, o, absum, rtol, growth, report: Report):
     floor = np.sqrt(np.mean(absum * absum)) if absum.ndim else 0.0
     scale = np.maximum(absum + floor, 1e-30)
     report.max_err[name] = float(np.max(err / scale)) if err.size else 0.0
-    bound = rtol * growth * scale
+    bound = tol * scale
     if not np.all(err <= bound):
         i = np.unravel_index(np.argmax(err - bound), np.shape(o)) if np.ndim(o) else ()
         raise AssertionError(f"{name}: gpu={np.asarray(g)[i]!r} oracle={np.asarray(o)[i]!r} "
-                             f"abs-sum={np.asarray(absum)[i]!r} allowed {rtol * growth:.3g}")
+                             f"abs-sum={np.asarray(absum)[i]!r} allowed {tol:.3g}")
 
 
 def compare(case: Case, gpu: dict) -> Report:
@@ -259,16 +281,18 @@ def compare(case: Case, gpu: dict) -> Report:
     assert np.array_equal(gpu["S"], rec["S"])
     assert set(np.unique(gpu["S"])).issubset({0.0, 1.0})
     og = oracle_grads(case, rec)
-    gr = horizon_growth(cfg, case.alpha, case.beta)
+    e32 = fp32_errors(case, rec, og)
+    rep.fp32 = e32
     if gpu["H"] is not None:
-        close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, gr, rep)
+        close_elementwise("v_soma", gpu["H"], rec["H"], RTOL_F32, tolerance(RTOL_F32, e32["v_soma"]), rep)
     rt_io = RTOL_BF16 if cfg.io == "bf16" else RTOL_F32
-    close_elementwise("grad_x", gpu["gX"], og["gX"], rt_io, gr, rep)
+    close_elementwise("grad_x", gpu["gX"], og["gX"], rt_io, tolerance(rt_io, e32["grad_x"]), rep)
     for k in ("g_kappa", "g_xi", "g_zeta"):
-        close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, gr, rep)
+        close_summed(k, gpu[k], og[k], og["abs_" + k[2:]], RTOL_F32, tolerance(RTOL_F32, e32[k]), rep)
     close_summed("g_alpha", gpu["g_alpha"], og["g_alpha"] if cfg.stateful else 0.0,
-                 og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, gr, rep)
-    close_summed("g_beta", gpu["g_beta"], og["g_beta"], og["abs_beta"], RTOL_F32, gr, rep)
+                 og["abs_alpha"] if cfg.stateful else 1.0, RTOL_F32, tolerance(RTOL_F32, e32["g_alpha"]), rep)
+    close_summed("g_beta", gpu["g_beta"], og["g_beta"], og["abs_beta"], RTOL_F32,
+                 tolerance(RTOL_F32, e32["g_beta"]), rep)
     if case.mask is not None:
         off = case.mask == 0
         off_c = np.repeat(off, cfg.comps_per_branch, axis=1)   # per compartment

@@ -242,3 +242,31 @@ def test_sample_slice_limit(lib):
     ok = base_cfg(T=2, batch=2, C=255, S=1 << 20, B=4, ckpt_every=1)
     assert lib.dendsn_ckpt_bytes(ctypes.byref(ok), ctypes.byref(out)) == 0
     assert out.value == 2 * 255 * (1 << 20) * 5 * 4   # one checkpoint: N (P + 1) floats, N = 2 C S
+
+
+def test_python_backward_checks_the_checkpoint_buffer():
+    """backward() refuses a checkpoint buffer that is missing, of another dtype or
+    smaller than this layer's dendsn_ckpt_bytes, before anything is launched (the
+    C ABI cannot see a buffer's size).  Host tensors: validation only."""
+    import torch
+
+    cfg = dendsn.DendSNConfig(T=8, batch=2, C=16, S=1, B=4, ckpt_every=4)
+    need = dendsn.dendsn_ckpt_bytes(cfg)
+    assert need > 0
+    x = torch.zeros((cfg.T, cfg.N, cfg.P))
+    alpha, kappa = torch.zeros(1), torch.zeros((cfg.C, cfg.B))
+    gS = torch.zeros((cfg.T, cfg.N))
+    call = lambda ck: dendsn.backward(cfg, x, alpha, kappa, None, None, None, ck, gS)
+    with pytest.raises(ValueError, match="required"):
+        call(None)
+    with pytest.raises(ValueError, match="bytes"):
+        call(torch.zeros(need // 4 - 1))                       # one float short
+    with pytest.raises(ValueError, match="float32"):
+        call(torch.zeros(need // 8, dtype=torch.float64))
+    with pytest.raises(ValueError, match="float32"):
+        call(torch.zeros(need // 2)[::2])                      # not contiguous
+    # a longer-horizon cfg needs more checkpoint bytes than this one's buffer holds
+    longer = cfg.with_(T=16)
+    with pytest.raises(ValueError, match="bytes"):
+        dendsn.backward(longer, torch.zeros((16, cfg.N, cfg.P)), alpha, kappa, None, None, None,
+                        torch.zeros(need // 4), torch.zeros((16, cfg.N)))
