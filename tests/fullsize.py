@@ -1,8 +1,10 @@
 """Per-batch-item oracle check for the full-size parity tests (runs in worker
 processes).  Neurons of different batch items are independent in both
 directions, so item b of a layer is checked on its own: spikes (forced-spike
-protocol), v_soma and grad_x element by element, and the item's parameter-
-gradient contributions are returned to be summed over all items in float64."""
+protocol) and the norm-wise errors of v_soma and grad_x; their elementwise
+errors, the kernel's and a plain float32 evaluation's, and the item's
+parameter-gradient contributions are returned, to be judged and summed over all
+items (judge_elementwise; sums in float64)."""
 
 from __future__ import annotations
 
@@ -58,19 +60,16 @@ def check_item(job: dict) -> dict:
                              stateful=p["stateful"], residual=p["residual"], k=p["k"], sg=p["sg"],
                              sg_scale=p["sg_scale"], detach=p["detach"])
     out = dict(item=b, error=None, exempt=exempt)
-    # elementwise comparisons of this item's outputs (scale: |o| + rms over the item)
+    # elementwise errors of this item's outputs (scale: |o| + rms over the item),
+    # the kernel's and the float32 evaluation's; judged over all items together
+    # (judge_elementwise), since a bound is set by the whole tensor's worst element
     for name, got, ref, f32, rtol in (("v_soma", H_g, rec["H"], r32["H"], RTOL_F32),
                                       ("grad_x", gX_g, g["gX"], r32["gX"], job["rtol_io"])):
-        scale = np.abs(ref) + np.sqrt(np.mean(ref * ref))
-        ratio = float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-300)))
-        tol = tolerance(rtol, fp32_eval.elementwise_ratio(f32, ref))
-        out["max_" + name] = ratio
-        if ratio > tol:
-            out["error"] = f"item {b}: {name} error/scale {ratio:.3e} > {tol:.3g}"
-            return out
+        out["gpu_" + name] = fp32_eval.elementwise_ratio(got, ref)
+        out["fp32_" + name] = fp32_eval.elementwise_ratio(f32, ref)
         den = np.linalg.norm(ref)
         nrel = float(np.linalg.norm(got - ref) / den) if den > 0 else 0.0
-        if nrel > (RTOL_F32 if name == "v_soma" else job["rtol_io"]):
+        if nrel > rtol:
             out["error"] = f"item {b}: {name} norm-wise error {nrel:.3e}"
             return out
     for k in ("kappa", "xi", "zeta", "alpha", "beta"):
@@ -78,3 +77,19 @@ def check_item(job: dict) -> dict:
         out["abs_" + k] = g["abs_" + k]
         out["f32_" + k] = r32["g_" + k]      # this item's float32 sums
     return out
+
+
+def judge_elementwise(res: list, rtol_io: float) -> list:
+    """The elementwise bounds over all checked items: the kernel's worst element
+    of each tensor against tolerance(rtol, the float32 evaluation's worst element
+    of the same tensor).  Returns the failures (empty when every bound holds)."""
+    errors = []
+    for name, rtol in (("v_soma", RTOL_F32), ("grad_x", rtol_io)):
+        gpu = max(r["gpu_" + name] for r in res)
+        e32 = max(r["fp32_" + name] for r in res)
+        tol = tolerance(rtol, e32)
+        if gpu > tol:
+            worst = max(res, key=lambda r: r["gpu_" + name])["item"]
+            errors.append(f"{name}: worst error/scale {gpu:.3e} (item {worst}) > {tol:.3g} "
+                          f"(float32 evaluation: {e32:.3e})")
+    return errors

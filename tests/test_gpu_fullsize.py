@@ -3,8 +3,9 @@ bench.py times (same cfg, automatic batch groups): every batch item's spikes,
 v_soma and grad_x are checked against the float64 oracle, run item by item in a
 pool of host processes, and the parameter gradients against the oracle's sums
 over all items.  Inputs are the benchmark's own seeded draws.  Tolerances are
-those of tests/parity.py: rtol, or 1.5 times the error of a plain float32
-evaluation of the same item where float32 itself cannot reach rtol."""
+those of tests/parity.py: rtol, or twice the error of a plain float32
+evaluation of the same items where float32 itself cannot reach rtol (each
+tensor's worst element over all items against the float32 evaluation's)."""
 
 import multiprocessing as mp
 import os
@@ -14,7 +15,7 @@ import pytest
 
 import paper_2412_06355_amd as dendsn
 import workloads
-from tests.fullsize import check_item
+from tests.fullsize import check_item, judge_elementwise
 from tests import fp32_eval
 from tests.parity import RTOL_BF16, RTOL_F32, announce, tolerance
 
@@ -67,7 +68,12 @@ def _check_against_oracle(wl, cfg, X, gS, kappa, alpha, p, mask_np, xg_files, tm
     errors = [r["error"] for r in res if r["error"]]
     assert not errors, errors[:5]
     exempt = sum(r["exempt"] for r in res)
-    announce(f"full-size parity {label}: {wl.batch} items, {exempt} near-threshold exemptions")
+    announce(f"full-size parity {label}: {wl.batch} items, {exempt} near-threshold exemptions; worst elementwise "
+             f"error/scale: v_soma {max(r['gpu_v_soma'] for r in res):.2e} (float32 evaluation "
+             f"{max(r['fp32_v_soma'] for r in res):.2e}), grad_x {max(r['gpu_grad_x'] for r in res):.2e} "
+             f"(float32 evaluation {max(r['fp32_grad_x'] for r in res):.2e})")
+    errors = judge_elementwise(res, rtol_io)
+    assert not errors, errors
 
     def summed(key):
         return sum(r[key] for r in res)

@@ -5,12 +5,13 @@ oracle, on the layers the GPU parity tests use.
 - The float32 evaluation computes the same function as the oracle: on short
   layers it agrees to float32 rounding (a dropped term or a wrong sign in it
   would show as an O(1) error).
-- On four-step layers with alpha = beta = 1/2 float32 meets rtol = 1e-5 with
-  room to spare, so their bound is rtol itself.
+- On four-step layers with alpha = beta = 1/2 float32 meets rtol = 1e-5, so
+  their bound is rtol (or, for the cifar-shaped grad_x where float32 reaches
+  5.3e-6, barely above it).
 - On the long-horizon layer (T = 64, alpha = 0.8, beta = 0.9) float32 cannot
   reach rtol on grad_x: the measured error is about 2.7e-5, so the bound there
-  is 1.5 times that (about 4e-5), where a formula over the chains' memories
-  had allowed 1.25e-4.
+  is twice that (about 5.4e-5), where a formula over the chains' memories had
+  allowed 1.25e-4.
 - The full-size harness (tests/fullsize.py) passes a float32-accurate result
   and rejects one with a planted error.
 """
@@ -57,8 +58,8 @@ def test_fp32_evaluation_computes_the_oracles_function(variant):
 def test_fp32_meets_rtol_on_four_step_layers(shape):
     e = _errors(_cfg(**shape), seed=7, x_std=0.5, random_affine=False)
     for k, v in e.items():
-        assert FP32_MARGIN * v <= RTOL_F32, (k, v)
-        assert tolerance(RTOL_F32, v) == RTOL_F32
+        assert v < RTOL_F32, (k, v)
+        assert tolerance(RTOL_F32, v) <= FP32_MARGIN * RTOL_F32
 
 
 def test_long_horizon_needs_more_than_rtol_in_fp32():
@@ -68,7 +69,7 @@ def test_long_horizon_needs_more_than_rtol_in_fp32():
     # grad_x: the adjoint of two leaky chains over 64 steps, through a steep surrogate
     assert 1.5e-5 < e["grad_x"] < 5e-5, e["grad_x"]
     tol = tolerance(RTOL_F32, e["grad_x"])
-    assert tol == FP32_MARGIN * e["grad_x"] and tol < 7.5e-5
+    assert tol == FP32_MARGIN * e["grad_x"] and tol < 1e-4
     # the potential itself and the summed gradients stay inside rtol
     for k in ("v_soma", "g_kappa", "g_xi", "g_zeta", "g_alpha", "g_beta"):
         assert tolerance(RTOL_F32, e[k]) == RTOL_F32, (k, e[k])
@@ -85,7 +86,7 @@ def _write(path, a):
 def test_full_size_harness_accepts_fp32_and_rejects_a_planted_error(tmp_path, plant):
     """check_item on one batch item whose 'kernel' outputs come from the float32
     evaluation: it must pass; with one grad_x element off by 3x its bound, fail."""
-    from tests.fullsize import check_item
+    from tests.fullsize import check_item, judge_elementwise
 
     c = _cfg(T=16, batch=2, C=64, S=1, B=8, beta=0.9, ckpt_every=4)
     case = make_case(c, seed=5, x_mean=0.1, alpha=0.8, random_affine=False)
@@ -109,7 +110,9 @@ def test_full_size_harness_accepts_fp32_and_rejects_a_planted_error(tmp_path, pl
                   C=c.C, S=c.S, psi=c.psi, stateful=c.stateful, residual=False, k=1, sg=c.sg,
                   sg_scale=c.sg_scale, detach=False)
     res = check_item(dict(item=1, M=c.C * c.S, T=c.T, params=params, rtol_io=RTOL_F32, **files))
+    assert res["error"] is None, res["error"]
+    errors = judge_elementwise([res], RTOL_F32)
     if plant:
-        assert res["error"] and "grad_x" in res["error"]
+        assert errors and "grad_x" in errors[0]
     else:
-        assert res["error"] is None, res["error"]
+        assert not errors, errors
