@@ -46,8 +46,9 @@
  *
  * Conventions:
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
- *     allocates nothing, keeps no state between calls and never synchronises:
- *     both calls enqueue kernels on the given stream and return.
+ *     allocates nothing, keeps no state between calls (the scratch array of
+ *     dendsn_backward_noalloc aside) and never synchronises: every call enqueues
+ *     kernels on the given stream and returns.
  *   - X, grad_x, ckpt and workspace must be 16-byte aligned; every other tensor
  *     must be aligned to its element size.
  *   - Outputs are overwritten, never accumulated.
@@ -176,6 +177,36 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
                               float* grad_alpha, float* grad_beta, float* grad_kappa,
                               float* grad_xi, float* grad_zeta, void* workspace,
                               size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Maximum workspace of dendsn_backward_noalloc: 16 MiB of device memory per
+ * GPU, held by the library from the first call on that GPU until the process
+ * ends (every benchmark-sized layer needs at most 12.1 MiB).
+ */
+#define DENDSN_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * dendsn_backward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, outputs and bit-identical results, without a workspace.
+ * The parameter-gradient partials go to a scratch array of
+ * DENDSN_NOALLOC_SCRATCH_BYTES that the library keeps in each GPU's memory;
+ * nothing is allocated by the call.  The call runs on the current device, and
+ * `stream` must belong to it (else DENDSN_E_INVALID).
+ *   - A layer whose dendsn_bwd_workspace_bytes exceeds the scratch size is
+ *     refused with DENDSN_E_WORKSPACE before anything is launched.
+ *   - Every call on one GPU shares that GPU's scratch array.  Calls that may
+ *     overlap on one GPU (several streams or host threads) race on it: the
+ *     caller serialises them.  Each call writes every scratch byte it reads, so
+ *     what an earlier call left there does not matter.
+ */
+dendsn_status dendsn_backward_noalloc(const dendsn_cfg* cfg, const void* x, const float* alpha,
+                                      const float* beta, const float* kappa, const float* xi,
+                                      const float* zeta, const uint8_t* mask, const float* ckpt,
+                                      const void* grad_spikes, const float* grad_v_soma,
+                                      void* grad_x, float* grad_alpha, float* grad_beta,
+                                      float* grad_kappa, float* grad_xi, float* grad_zeta,
+                                      hipStream_t stream);
 
 /* Static name of a status code. */
 const char* dendsn_status_str(dendsn_status status);

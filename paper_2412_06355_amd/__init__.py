@@ -8,10 +8,12 @@ of include/dendsn.h.  This package is the Python binding of that library.
 from .binding import (  # noqa: F401
     EXPORTS,
     LIB_PATH,
+    NOALLOC_SCRATCH_BYTES,
     DendSNConfig,
     DendSNError,
     backward,
     dendsn_backward,
+    dendsn_backward_noalloc,
     dendsn_bwd_workspace_bytes,
     dendsn_ckpt_bytes,
     dendsn_forward,

@@ -22,6 +22,8 @@ PSI = {"identity": 0, "mexhat": 1}
 SG = {"atan": 0, "sigmoid": 1}
 LAYOUT = {"npb": 0, "channel_major": 1}
 
+NOALLOC_SCRATCH_BYTES = 16 << 20   # DENDSN_NOALLOC_SCRATCH_BYTES of include/dendsn.h
+
 STATUS = {0: "DENDSN_OK", 1: "DENDSN_E_INVALID", 2: "DENDSN_E_UNSUPPORTED",
           3: "DENDSN_E_WORKSPACE", 4: "DENDSN_E_HIP"}
 
@@ -111,6 +113,7 @@ _SIGS = {
     "dendsn_forward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 11),
     "dendsn_backward": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 17
                         + [ctypes.c_size_t, ctypes.c_void_p]),
+    "dendsn_backward_noalloc": (ctypes.c_int, [ctypes.POINTER(dendsn_cfg)] + [ctypes.c_void_p] * 17),
     "dendsn_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "dendsn_last_error": (ctypes.c_char_p, []),
 }
@@ -191,6 +194,17 @@ def dendsn_backward(cfg: DendSNConfig, x, alpha, beta, kappa, xi, zeta, mask, ck
                                  _ptr(grad_x), _ptr(grad_alpha), _ptr(grad_beta), _ptr(grad_kappa),
                                  _ptr(grad_xi), _ptr(grad_zeta), _ptr(workspace), ctypes.c_size_t(ws_bytes),
                                  st))
+
+
+def dendsn_backward_noalloc(cfg: DendSNConfig, x, alpha, beta, kappa, xi, zeta, mask, ckpt, grad_spikes,
+                            grad_v_soma, grad_x, grad_alpha, grad_beta, grad_kappa, grad_xi, grad_zeta,
+                            stream=None):
+    c = cfg.to_c()
+    st = stream if stream is not None else _stream(x.device)
+    _check(lib().dendsn_backward_noalloc(ctypes.byref(c), _ptr(x), _ptr(alpha), _ptr(beta), _ptr(kappa),
+                                         _ptr(xi), _ptr(zeta), _ptr(mask), _ptr(ckpt), _ptr(grad_spikes),
+                                         _ptr(grad_v_soma), _ptr(grad_x), _ptr(grad_alpha), _ptr(grad_beta),
+                                         _ptr(grad_kappa), _ptr(grad_xi), _ptr(grad_zeta), st))
 
 
 # ---------------------------------------------------------------------------

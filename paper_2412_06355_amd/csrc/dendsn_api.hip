@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "dendsn.h"
@@ -443,13 +444,58 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   return DENDSN_OK;
 }
 
-dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* beta,
-                              const float* kappa, const float* xi, const float* zeta, const uint8_t* mask,
-                              const float* ckpt, const void* grad_spikes, const float* grad_v_soma,
-                              void* grad_x, float* grad_alpha, float* grad_beta, float* grad_kappa,
-                              float* grad_xi, float* grad_zeta, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream) {
-  g_last_error.clear();
+}  // extern "C"
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// The allocation-free backward's workspace: a device array of this module,
+// one copy per GPU (each device that loads the library holds its own), whose
+// address on the current device is looked up once per device.  Host code never
+// passes `scratch` itself (in host code that name is a stand-in, not a device
+// address); it passes the looked-up pointer.  The backward writes every partial
+// slot it later reads within the call, so nothing needs clearing between calls.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = DENDSN_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+dendsn_status scratch_on_stream_device(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("hipStreamGetDevice: ") + hipGetErrorString(e));
+    if (int(sdev) != dev)
+      return fail(DENDSN_E_INVALID, "stream belongs to another device than the current one");
+  }
+  if (dev < 0 || dev >= kMaxDevices) return fail(DENDSN_E_UNSUPPORTED, "device index above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(DENDSN_E_HIP, std::string("scratch address: ") + hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return DENDSN_OK;
+}
+
+// The backward on the caller's workspace or, with own_scratch, on the
+// library's scratch array of the stream's device (every argument is checked
+// before the array's address is looked up).
+dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* beta,
+                            const float* kappa, const float* xi, const float* zeta, const uint8_t* mask,
+                            const float* ckpt, const void* grad_spikes, const float* grad_v_soma, void* grad_x,
+                            float* grad_alpha, float* grad_beta, float* grad_kappa, float* grad_xi,
+                            float* grad_zeta, void* workspace, size_t workspace_bytes, bool own_scratch,
+                            hipStream_t stream) {
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
   if (!x) return fail(DENDSN_E_INVALID, "x is NULL");
@@ -471,11 +517,19 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
   size_t offA, total;
   ws_layout(cfg, p, &offA, &total);
-  if (!workspace) return fail(DENDSN_E_WORKSPACE, "workspace is NULL");
-  if (!aligned(workspace, 16)) return fail(DENDSN_E_WORKSPACE, "workspace must be 16-byte aligned");
-  if (workspace_bytes < total)
-    return fail(DENDSN_E_WORKSPACE, "workspace smaller than dendsn_bwd_workspace_bytes()");
+  if (own_scratch) {
+    if (total > kScratchBytes)
+      return fail(DENDSN_E_WORKSPACE, "layer needs " + std::to_string(total) +
+                                          " workspace bytes, above the allocation-free scratch of " +
+                                          std::to_string(kScratchBytes));
+  } else {
+    if (!workspace) return fail(DENDSN_E_WORKSPACE, "workspace is NULL");
+    if (!aligned(workspace, 16)) return fail(DENDSN_E_WORKSPACE, "workspace must be 16-byte aligned");
+    if (workspace_bytes < total)
+      return fail(DENDSN_E_WORKSPACE, "workspace smaller than dendsn_bwd_workspace_bytes()");
+  }
   if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
+  if (own_scratch && (st = scratch_on_stream_device(stream, &workspace)) != DENDSN_OK) return st;
 
   BwdArgs ba;
   memset(&ba, 0, sizeof(ba));
@@ -521,6 +575,33 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
   e = hipGetLastError();
   if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("finalize launch: ") + hipGetErrorString(e));
   return DENDSN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float* alpha, const float* beta,
+                              const float* kappa, const float* xi, const float* zeta, const uint8_t* mask,
+                              const float* ckpt, const void* grad_spikes, const float* grad_v_soma,
+                              void* grad_x, float* grad_alpha, float* grad_beta, float* grad_kappa,
+                              float* grad_xi, float* grad_zeta, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  g_last_error.clear();
+  return backward_impl(cfg, x, alpha, beta, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma, grad_x,
+                       grad_alpha, grad_beta, grad_kappa, grad_xi, grad_zeta, workspace, workspace_bytes, false,
+                       stream);
+}
+
+dendsn_status dendsn_backward_noalloc(const dendsn_cfg* cfg, const void* x, const float* alpha,
+                                      const float* beta, const float* kappa, const float* xi, const float* zeta,
+                                      const uint8_t* mask, const float* ckpt, const void* grad_spikes,
+                                      const float* grad_v_soma, void* grad_x, float* grad_alpha,
+                                      float* grad_beta, float* grad_kappa, float* grad_xi, float* grad_zeta,
+                                      hipStream_t stream) {
+  g_last_error.clear();
+  return backward_impl(cfg, x, alpha, beta, kappa, xi, zeta, mask, ckpt, grad_spikes, grad_v_soma, grad_x,
+                       grad_alpha, grad_beta, grad_kappa, grad_xi, grad_zeta, nullptr, 0, true, stream);
 }
 
 }  // extern "C"

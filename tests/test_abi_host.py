@@ -270,3 +270,29 @@ def test_python_backward_checks_the_checkpoint_buffer():
     with pytest.raises(ValueError, match="bytes"):
         dendsn.backward(longer, torch.zeros((16, cfg.N, cfg.P)), alpha, kappa, None, None, None,
                         torch.zeros(need // 4), torch.zeros((16, cfg.N)))
+
+
+def bwd_noalloc(lib, cfg, ckpt=None, x=GOOD, gx=GOOD + 0x400, gs=GOOD + 0x500):
+    p = lambda v: None if v is None else fake(v)
+    return lib.dendsn_backward_noalloc(ctypes.byref(cfg), p(x), p(GOOD + 0x100), None, p(GOOD + 0x200), None,
+                                       None, None, p(ckpt), p(gs), None, p(gx), None, None, None, None, None,
+                                       None)
+
+
+def test_noalloc_backward_argument_checks(lib):
+    """The allocation-free backward checks its arguments like dendsn_backward, and
+    refuses a layer whose partials exceed its scratch array, all before any HIP
+    call (no device is needed to reach these refusals)."""
+    cfg = base_cfg(T=8, ckpt_every=4)
+    assert bwd_noalloc(lib, cfg, ckpt=None) == E_INVALID
+    assert bwd_noalloc(lib, cfg, ckpt=GOOD + 0x800, x=None) == E_INVALID
+    assert bwd_noalloc(lib, cfg, ckpt=GOOD + 0x800, gx=GOOD + 0x404) == E_INVALID
+    big = base_cfg(T=4, batch=128, C=65536, S=1, B=32)
+    need = ctypes.c_size_t(0)
+    assert lib.dendsn_bwd_workspace_bytes(ctypes.byref(big), ctypes.byref(need)) == OK
+    assert need.value > dendsn.NOALLOC_SCRATCH_BYTES
+    assert bwd_noalloc(lib, big) == E_WORKSPACE
+    assert "scratch" in dendsn.dendsn_last_error()
+    # the binding's size is the header's
+    m = re.search(r"#define DENDSN_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == dendsn.NOALLOC_SCRATCH_BYTES

@@ -1,0 +1,80 @@
+"""The allocation-free backward (dendsn_backward_noalloc, through the C ABI)
+against the workspace backward (dendsn_backward) on the same inputs: every
+output bit for bit, on two calls in a row, the second on a smaller layer (the
+scratch array then still holds the first call's partials)."""
+
+import numpy as np
+import pytest
+
+import paper_2412_06355_amd as dendsn
+from tests.parity import announce, make_case, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _cfg(**kw):
+    base = dict(T=4, batch=2, C=256, S=1, B=4, beta=0.5, v_th=1.0, psi="mexhat", sg="sigmoid", sg_scale=4.0)
+    base.update(kw)
+    return dendsn.DendSNConfig(**base)
+
+
+def _both(case, device):
+    """Forward once, then the backward through both entry points."""
+    import torch
+
+    cfg = case.cfg
+    d = to_device(case, device)
+    spikes, _, ckpt = dendsn.forward(cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"],
+                                     beta=d["beta"])
+    ref = dendsn.backward(cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"], ckpt, d["gS"],
+                          d["gV"], beta=d["beta"])
+    out = {k: torch.full_like(v, float("nan")) for k, v in ref.items()}
+    dendsn.dendsn_backward_noalloc(cfg, d["x"], d["alpha"], d["beta"], d["kappa"], d["xi"], d["zeta"], d["mask"],
+                                   ckpt, d["gS"], d["gV"], out["grad_x"], out["grad_alpha"], out["grad_beta"],
+                                   out["grad_kappa"], out["grad_xi"], out["grad_zeta"])
+    torch.cuda.synchronize(device)
+    return ref, out
+
+
+def _bits(t):
+    import torch
+
+    return t.contiguous().view(torch.uint8)
+
+
+def _assert_identical(ref, out):
+    import torch
+
+    for k in ref:
+        assert torch.equal(_bits(ref[k]), _bits(out[k])), k
+
+
+# a large layer first (12 MiB of partials: the gated fully connected shape),
+# then smaller ones of other tilings
+SEQUENCE = [
+    ("fc-gated-large", dict(T=4, batch=64, C=8192, S=1, B=32), dict(mask_rho=0.5)),
+    ("conv-small", dict(T=4, batch=2, C=16, S=1024, B=8), dict(random_affine=True)),
+    ("long-ckpt-smaller", dict(T=24, batch=2, C=64, S=1, B=16, ckpt_every=8, beta=0.9),
+     dict(x_mean=0.1, alpha=0.8, with_gv=True)),
+]
+
+
+def test_noalloc_backward_equals_workspace_backward(gpu_device):
+    for name, ckw, mkw in SEQUENCE:
+        cfg = _cfg(**ckw)
+        assert dendsn.dendsn_bwd_workspace_bytes(cfg) <= dendsn.NOALLOC_SCRATCH_BYTES
+        case = make_case(cfg, seed=3, name=f"noalloc/{name}", **mkw)
+        announce(f"noalloc {name}: {cfg}")
+        ref, out = _both(case, gpu_device)
+        _assert_identical(ref, out)
+
+
+def test_noalloc_twice_on_a_shrinking_layer(gpu_device):
+    """Two calls in a row, the second on a smaller layer of the same tiling."""
+    for name, batch in (("first", 6), ("second-smaller", 2)):
+        cfg = _cfg(T=8, batch=batch, C=96, S=300, B=8, ckpt_every=4)
+        case = make_case(cfg, seed=9 + batch, x_std=1.2, alpha=0.6, mask_rho=0.6, name=f"noalloc/{name}")
+        announce(f"noalloc {name}: {cfg}")
+        ref, out = _both(case, gpu_device)
+        _assert_identical(ref, out)
+        assert np.isfinite(out["grad_x"].float().cpu().numpy()).all()
