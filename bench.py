@@ -8,7 +8,10 @@ already resident in HBM when timing starts.  Prints one JSON line.
 The rate is neuron-branch-steps per second: T * N * B / (time of one step).
 The roofline object is for the dominant kernel (the backward scan): its
 algorithmic bytes per launch divided by its mean launch time, timed with HIP
-events on the stream the kernels run on, against MI355X's 8 TB/s HBM peak.
+events on the stream the kernels run on, each timed call preceded by an untimed
+512 MiB scratch read that evicts the MALL (so the bytes come from HBM), against
+MI355X's 8 TB/s HBM peak; the same calls back to back are reported as
+"unflushed".
 """
 
 from __future__ import annotations
@@ -25,7 +28,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-PROFILE_PMC = os.path.join(ROOT, "profiles", "pmc_dendsn_bwd_cifar.txt")
+FLUSH_BYTES = 512 << 20   # untimed scratch read before each per-launch timed call: evicts the 256 MB MALL
+
+
+def pmc_summary_path(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"pmc_dendsn_bwd_{workload}.txt")
 
 
 def kernel_source_digest() -> str:
@@ -40,12 +47,13 @@ def kernel_source_digest() -> str:
 
 
 def measured_traffic(digest: str, workload: str):
-    """HBM bytes per backward launch from a committed rocprofv3 counter summary,
-    or None when there is none for this workload or the kernels changed since."""
-    if not os.path.exists(PROFILE_PMC):
+    """HBM bytes per backward launch from the committed rocprofv3 counter summary
+    of this workload, or None when there is none or the kernels changed since."""
+    path = pmc_summary_path(workload)
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(PROFILE_PMC) as f:
+    with open(path) as f:
         for line in f:
             if "=" in line and not line.startswith("#"):
                 k, v = line.strip().split("=", 1)
@@ -202,22 +210,40 @@ def main():
     torch.cuda.synchronize(dev)
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
 
-    # per-launch timing of each kernel call, on the stream the kernels run on
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps * len(tasks))]
-    it = iter(evs)
-    torch.cuda.synchronize(dev)
-    for _ in range(args.steps):
-        for m in tasks:
-            e = next(it)
-            e[0].record(stream)
-            dendsn.dendsn_forward(cfg, X, alpha, None, kappa, None, None, m, spikes, None, ckpt)
-            e[1].record(stream)
-            dendsn.dendsn_backward(cfg, X, alpha, None, kappa, None, None, m, ckpt, gS, None, gX, g_alpha,
-                                   g_beta, g_kappa, g_xi, g_zeta, ws)
-            e[2].record(stream)
-    torch.cuda.synchronize(dev)
-    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / len(evs)
-    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / len(evs)
+    # per-launch timing of each kernel call, with HIP events on the stream the
+    # kernels run on.  Flushed (the default figures): before each timed call an
+    # untimed read of 512 MiB of scratch (twice the 256 MB MALL) evicts whatever
+    # the cache held, and writes back any dirty lines outside the timed region,
+    # so every byte a call reads comes from HBM.  Unflushed: the calls back to
+    # back, as in the whole step (a layer whose tensors fit the MALL may hit in it).
+    flush_buf = torch.zeros((FLUSH_BYTES // 4,), dtype=torch.float32, device=dev)
+
+    def timed_calls(flush: bool):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps * len(tasks))]
+        it = iter(evs)
+        torch.cuda.synchronize(dev)
+        for i in range(args.steps):
+            for m in tasks:
+                e = next(it)
+                if flush:
+                    flush_buf.sum()
+                e[0].record(stream)
+                dendsn.dendsn_forward(cfg, X, alpha, None, kappa, None, None, m, spikes, None, ckpt)
+                e[1].record(stream)
+                if flush:
+                    flush_buf.sum()
+                e[2].record(stream)
+                dendsn.dendsn_backward(cfg, X, alpha, None, kappa, None, None, m, ckpt, gS, None, gX, g_alpha,
+                                       g_beta, g_kappa, g_xi, g_zeta, ws)
+                e[3].record(stream)
+        torch.cuda.synchronize(dev)
+        fwd = sum(e[0].elapsed_time(e[1]) for e in evs) / len(evs)
+        bwd = sum(e[2].elapsed_time(e[3]) for e in evs) / len(evs)
+        return fwd, bwd
+
+    fwd_ms, bwd_ms = timed_calls(flush=True)
+    fwd_ms_nf, bwd_ms_nf = timed_calls(flush=False)
+    del flush_buf
 
     # sanity of the last outputs: spikes are exact 0/1, gradients finite
     sp = spikes.float()
@@ -258,9 +284,14 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "dendsn_backward (scan + finalize)",
                      "achieved": bwd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": bwd_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "algorithmic_bytes_per_launch": bwd_bytes, "ms_per_launch": bwd_ms},
+                     "algorithmic_bytes_per_launch": bwd_bytes, "ms_per_launch": bwd_ms,
+                     "timing": "512 MiB scratch read (MALL eviction) before each timed call",
+                     "unflushed": {"ms_per_launch": bwd_ms_nf,
+                                   "frac": bwd_bytes / (bwd_ms_nf * 1e-3) / 1e9 / HBM_PEAK_GBS}},
         "roofline_fwd": {"achieved": fwd_gbs, "frac": fwd_gbs / HBM_PEAK_GBS, "unit": "GB/s",
-                         "algorithmic_bytes_per_launch": fwd_bytes, "ms_per_launch": fwd_ms},
+                         "algorithmic_bytes_per_launch": fwd_bytes, "ms_per_launch": fwd_ms,
+                         "unflushed": {"ms_per_launch": fwd_ms_nf,
+                                       "frac": fwd_bytes / (fwd_ms_nf * 1e-3) / 1e9 / HBM_PEAK_GBS}},
         "step_hbm_frac": (fwd_bytes + bwd_bytes) * n_tasks / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "outputs_ok": ok,
         "firing_rate": rate,

@@ -117,9 +117,14 @@ typedef struct dendsn_cfg {
 
 /*
  * Size in bytes of the state-checkpoint buffer that dendsn_forward fills and
- * dendsn_backward reads: nck * N * (P + 1) * 4 with nck = ceil(T / K) - 1
- * (the dendritic state and the somatic potential after steps K, 2K, ... < T).
- * Zero when K >= T.  Returns DENDSN_E_INVALID / _UNSUPPORTED for a bad cfg.
+ * dendsn_backward reads: gradient checkpointing of the dendritic integration
+ * (Results, DendSNN efficiency paragraph: the backward recomputes the dendrite
+ * instead of storing it).  nck = ceil(T / K) - 1 checkpoints, the states after
+ * steps K, 2K, ... < T: nck * N * (P + 1) * 4 bytes for a stateful dendrite (the
+ * P compartment states and the somatic potential), nck * N * 4 for the
+ * Stateless Dendrite (only the somatic potential: its compartment state is the
+ * input itself).  Zero when K >= T.  Returns DENDSN_E_INVALID / _UNSUPPORTED
+ * for a bad cfg.
  */
 dendsn_status dendsn_ckpt_bytes(const dendsn_cfg* cfg, size_t* bytes);
 
@@ -154,7 +159,8 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
  * Backward scan: gradients of  sum(grad_spikes * S) + sum(grad_v_soma * H)  with
  * Theta'(H - v_th) replaced by the surrogate cfg->sg, through time (BPTT).
  * The dendrite is recomputed from x and the checkpoints (gradient
- * checkpointing); nothing else of the forward is stored.  The call must use the
+ * checkpointing of the dendritic integration; Results, DendSNN efficiency
+ * paragraph); nothing else of the forward is stored.  The call must use the
  * same cfg, x, alpha, beta, kappa, xi, zeta and mask as the forward that wrote ckpt.
  *   ckpt         required when nck > 0 (see dendsn_ckpt_bytes)
  *   grad_spikes  [T,N] io     required

@@ -330,10 +330,16 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   return p;
 }
 
+// Checkpoints: the compartment states (stateful dendrite only) and the somatic
+// potential after steps K, 2K, ... < T.
 size_t ckpt_bytes(const dendsn_cfg* c, const Plan& p) {
   const int64_t N = c->batch * c->C * c->S;
-  return size_t(p.nck) * size_t(N) * size_t(c->B * c->comps_per_branch + 1) * sizeof(float);
+  const size_t per_neuron = c->stateful ? size_t(c->B * c->comps_per_branch + 1) : 1;
+  return size_t(p.nck) * size_t(N) * per_neuron * sizeof(float);
 }
+
+// Runtime kernel variant (see variant_bits).
+int variant_of(const dendsn_cfg* c) { return c->psi | (c->residual << 1) | ((c->stateful ? 0 : 1) << 2); }
 
 void ws_layout(const dendsn_cfg* c, const Plan& p, size_t* offA, size_t* total) {
   const size_t nP = size_t(p.G) * size_t(p.tpc) * size_t(c->C) * size_t(2 * c->B + c->B * c->comps_per_branch);
@@ -433,8 +439,10 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   fill_scan(cfg, p, x, alpha, beta, kappa, xi, zeta, mask, &fa.s);
   fa.spikes = spikes;
   fa.vsoma = v_soma;
-  fa.ckpt = p.nck > 0 ? ckpt : nullptr;
-  const int v = cfg->psi | (cfg->residual << 1);
+  float* ck = p.nck > 0 ? ckpt : nullptr;
+  fa.ckpt = cfg->stateful ? ck : nullptr;
+  fa.ckh = ck ? ck + (cfg->stateful ? int64_t(p.nck) * fa.s.N * fa.s.P : 0) : nullptr;
+  const int v = variant_of(cfg);
   const bool bf = cfg->io == DENDSN_IO_BF16;
   const hipError_t e =
       p.cm ? (bf ? launch_fwd_bf16_cm(p, fa, v, stream) : launch_fwd_f32_cm(p, fa, v, stream))
@@ -534,7 +542,9 @@ dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* a
   BwdArgs ba;
   memset(&ba, 0, sizeof(ba));
   fill_scan(cfg, p, x, alpha, beta, kappa, xi, zeta, mask, &ba.s);
-  ba.ckpt = ckpt;
+  const float* ck = p.nck > 0 ? ckpt : nullptr;
+  ba.ckpt = cfg->stateful ? ck : nullptr;
+  ba.ckh = ck ? ck + (cfg->stateful ? int64_t(p.nck) * ba.s.N * ba.s.P : 0) : nullptr;
   ba.gspk = grad_spikes;
   ba.gv = grad_v_soma;
   // the single-chunk pipeline reads grad_v_soma through a buffer of gvn bytes:
@@ -549,7 +559,7 @@ dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* a
   ba.wide = ba.slots > kNarrowSlots;
   ba.detach = cfg->detach_reset;
   ba.sg_scale = cfg->sg_scale;
-  const int v = cfg->psi | (cfg->residual << 1);
+  const int v = variant_of(cfg);
   const bool bf = cfg->io == DENDSN_IO_BF16;
   hipError_t e;
   if (cfg->sg == DENDSN_SG_SIGMOID)

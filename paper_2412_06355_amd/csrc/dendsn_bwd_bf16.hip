@@ -1,6 +1,8 @@
 // Backward-kernel instantiations and dispatch for bf16 storage.
 // V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite,
 // bit 5 = sigmoid surrogate (DENDSN_SG); KS: stash steps.
+// Bit 6 of V = Stateless Dendrite (the runtime v passed in: psi | residual << 1 |
+// stateless << 2, mapped by variant_bits).
 #include "dendsn_kernels.h"
 
 #ifndef DENDSN_SG
@@ -13,12 +15,11 @@ constexpr int kVS = DENDSN_SG << 5;  // surrogate bit of the variant
 
 template <int BL, int L, int KS>
 static hipError_t launch_bwd_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
-  switch (v) {
-    case 0: dendsn_bwd_kernel<bf16_t, BL, L, kVS | 0, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<bf16_t, BL, L, kVS | 1, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<bf16_t, BL, L, kVS | 2, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<bf16_t, BL, L, kVS | 3, KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    default: return hipErrorInvalidValue;
+  switch (v & 7) {
+#define DENDSN_V(n) \
+    case n: dendsn_bwd_kernel<bf16_t, BL, L, kVS | variant_bits(n), KS><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    DENDSN_EACH_VARIANT(DENDSN_V)
+#undef DENDSN_V
   }
   return hipGetLastError();
 }

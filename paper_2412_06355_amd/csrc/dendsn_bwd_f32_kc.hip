@@ -2,6 +2,8 @@
 // compartments per branch (stash capacity 4).  V: bit 0 = Mexican-hat
 // activation, bit 1 = residual dendrite, bits 2-3 = log2(KC), bit 5 = sigmoid
 // surrogate (DENDSN_SG).
+// Bit 6 of V = Stateless Dendrite (the runtime v passed in: psi | residual << 1 |
+// stateless << 2, mapped by variant_bits).
 #include "dendsn_kernels.h"
 
 #ifndef DENDSN_SG
@@ -15,11 +17,11 @@ constexpr int kVS = DENDSN_SG << 5;  // surrogate bit of the variant
 template <int BL, int L, int KC>
 static hipError_t launch_bwd_kc_v(const dim3& grid, const BwdArgs& ba, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = (KC == 2 ? 1 : 2) << 2;
-  switch (v & 3) {
-    case 0: dendsn_bwd_kernel<float, BL, L, kVS | VK | 0, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 1: dendsn_bwd_kernel<float, BL, L, kVS | VK | 1, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 2: dendsn_bwd_kernel<float, BL, L, kVS | VK | 2, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
-    case 3: dendsn_bwd_kernel<float, BL, L, kVS | VK | 3, 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+  switch (v & 7) {
+#define DENDSN_V(n) \
+    case n: dendsn_bwd_kernel<float, BL, L, kVS | VK | variant_bits(n), 4><<<grid, dim3(kThreads), lds, stream>>>(ba); break;
+    DENDSN_EACH_VARIANT(DENDSN_V)
+#undef DENDSN_V
   }
   return hipGetLastError();
 }

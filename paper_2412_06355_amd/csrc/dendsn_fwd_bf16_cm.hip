@@ -2,6 +2,8 @@
 // channel-major layout (X / grad_x [T, batch, C, P, S]).
 // V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite, bits 2-3 =
 // log2(KC), bit 4 = channel-major.
+// Bit 6 of V = Stateless Dendrite (the runtime v passed in: psi | residual << 1 |
+// stateless << 2, mapped by variant_bits).
 #include "dendsn_kernels.h"
 
 namespace dendsn {
@@ -9,11 +11,11 @@ namespace dendsn {
 template <int BL, int L, int KC>
 static hipError_t launch_fwd_cm_v(const dim3& grid, const FwdArgs& fa, int v, size_t lds, hipStream_t stream) {
   constexpr int VK = 16 | ((KC == 1 ? 0 : (KC == 2 ? 1 : 2)) << 2);
-  switch (v & 3) {
-    case 0: dendsn_fwd_kernel<bf16_t, BL, L, VK | 0><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 1: dendsn_fwd_kernel<bf16_t, BL, L, VK | 1><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 2: dendsn_fwd_kernel<bf16_t, BL, L, VK | 2><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 3: dendsn_fwd_kernel<bf16_t, BL, L, VK | 3><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+  switch (v & 7) {
+#define DENDSN_V(n) \
+    case n: dendsn_fwd_kernel<bf16_t, BL, L, VK | variant_bits(n)><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    DENDSN_EACH_VARIANT(DENDSN_V)
+#undef DENDSN_V
   }
   return hipGetLastError();
 }

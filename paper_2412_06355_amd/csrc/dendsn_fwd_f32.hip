@@ -1,17 +1,18 @@
 // Forward-kernel instantiations and dispatch for f32 storage.
 // V: bit 0 = Mexican-hat activation, bit 1 = residual dendrite.
+// Bit 6 of V = Stateless Dendrite (the runtime v passed in: psi | residual << 1 |
+// stateless << 2, mapped by variant_bits).
 #include "dendsn_kernels.h"
 
 namespace dendsn {
 
 template <int BL, int L>
 static hipError_t launch_fwd_v(const dim3& grid, const FwdArgs& fa, int v, size_t lds, hipStream_t stream) {
-  switch (v) {
-    case 0: dendsn_fwd_kernel<float, BL, L, 0><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 1: dendsn_fwd_kernel<float, BL, L, 1><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 2: dendsn_fwd_kernel<float, BL, L, 2><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    case 3: dendsn_fwd_kernel<float, BL, L, 3><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
-    default: return hipErrorInvalidValue;
+  switch (v & 7) {
+#define DENDSN_V(n) \
+    case n: dendsn_fwd_kernel<float, BL, L, variant_bits(n)><<<grid, dim3(kThreads), lds, stream>>>(fa); break;
+    DENDSN_EACH_VARIANT(DENDSN_V)
+#undef DENDSN_V
   }
   return hipGetLastError();
 }

@@ -31,13 +31,16 @@ typedef uint16_t bf16_t;  // bf16 storage
 // residual dendrite (Z also receives the mean synaptic input of the neuron),
 // bits 2-3 = log2 of the compartments per branch KC (1, 2 or 4), bit 4 =
 // channel-major X / grad_x ([T, batch, C, P, S]: a neuron's compartments S
-// elements apart).  A lane holds BL branches, i.e. E = BL * KC compartments of
-// its neuron.
+// elements apart), bit 6 = Stateless Dendrite (a compartment's state is its
+// input of the step: no leak, no dendritic state across steps or checkpoints,
+// no adjoint recurrence and no alpha gradient).  A lane holds BL branches,
+// i.e. E = BL * KC compartments of its neuron.
 template <int V> constexpr bool kMH = (V & 1) != 0;
 template <int V> constexpr bool kRes = (V & 2) != 0;
 template <int V> constexpr int kKC = 1 << ((V >> 2) & 3);
 template <int V> constexpr bool kCM = (V & 16) != 0;
 template <int V> constexpr int kSG = (V >> 5) & 1;  // backward only: dendsn_sg surrogate
+template <int V> constexpr bool kSL = (V & 64) != 0;
 // Forward over bf16 rows without the residual dendrite: the branch gate is applied
 // while the raw rows are widened (the residual sums every compartment's input,
 // gated or not).  Measured: forward 2-2.5 % faster; the backward kept its
@@ -543,7 +546,7 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL * kKC<V>], const f
   for (int j = 0; j < BL; ++j) {
 #pragma unroll
     for (int i = j * KC; i < (j + 1) * KC; ++i) {
-      float v = fmaf(alpha, vd[i], xv[i]);   // alpha = 0: Stateless Dendrite
+      const float v = kSL<V> ? xv[i] : fmaf(alpha, vd[i], xv[i]);
       vd[i] = (kGated || br.on[j]) ? v : 0.0f;
     }
     // KC = 1: the signed (Vd - xi)/zeta, u = |tt|; else u = ||Vd - xi|| / zeta >= 0
@@ -735,7 +738,7 @@ struct FwdLane {
   int kc;         // steps until the next checkpoint
   IO* sp;         // spikes row t of this batch item
   float* vp;      // v_soma row t (or null)
-  float* ckv;     // next checkpoint's dendritic-state block of this item
+  float* ckv;     // next checkpoint's dendritic-state block of this item (stateful dendrite)
   float* ckh;     // next checkpoint's H row of this item
 };
 
@@ -747,7 +750,7 @@ __device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, Fw
   st.sp = static_cast<IO*>(fa.spikes) + n0;
   st.vp = fa.vsoma ? fa.vsoma + n0 : nullptr;
   st.ckv = fa.ckpt ? fa.ckpt + n0 * a.P : nullptr;
-  st.ckh = fa.ckpt ? fa.ckpt + int64_t(a.nck) * a.N * a.P + n0 : nullptr;
+  st.ckh = fa.ckh ? fa.ckh + n0 : nullptr;
 #pragma unroll
   for (int j = 0; j < E; ++j) st.vd[j] = 0.0f;
   st.h = 0.0f;
@@ -776,10 +779,12 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
       }
       if (--st.kc == 0) {
         st.kc = a.K;
-        if (st.ckv && t + 1 < T) {
-          store_vec<E>(at(st.ckv, lo.c), st.vd);
+        if (st.ckh && t + 1 < T) {
+          if constexpr (!kSL<V>) {  // the Stateless Dendrite has no state to keep
+            store_vec<E>(at(st.ckv, lo.c), st.vd);
+            st.ckv += a.N * a.P;
+          }
           if (lead) *at(st.ckh, lo.v) = st.h;
-          st.ckv += a.N * a.P;
           st.ckh += a.N;
         }
       }
@@ -944,18 +949,17 @@ struct SegStart {
   float h;
 };
 
-template <typename IO, int E>
+template <typename IO, int E, bool SL>
 __device__ __forceinline__ void load_seg_start(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int seg,
                                                SegStart<E>& st) {
   const ScanArgs& a = ba.s;
-  if (seg == 0) {
+  if (seg == 0 || SL) {  // the Stateless Dendrite restarts from its input: no state to load
 #pragma unroll
     for (int j = 0; j < E; ++j) st.v[j] = 0.0f;
-    st.h = 0.0f;
   } else {
     load_vec<E>(at(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.P, lo.c), st.v);
-    st.h = __builtin_nontemporal_load(at(ba.ckpt + int64_t(a.nck) * a.N * a.P + int64_t(seg - 1) * a.N + n0, lo.v));
   }
+  st.h = seg == 0 ? 0.0f : __builtin_nontemporal_load(at(ba.ckh + int64_t(seg - 1) * a.N + n0, lo.v));
 }
 
 // Registers a chunk's recompute leaves for its adjoint pass: the dendritic
@@ -1029,12 +1033,12 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
           y = fabsf(tt);
           r = tt > 0.0f ? dhk : (tt < 0.0f ? -dhk : 0.0f);
         }
-        bl.lam[j] = fmaf(alpha, bl.lam[j], r);
+        bl.lam[j] = kSL<V> ? r : fmaf(alpha, bl.lam[j], r);
         gxo[j] = kRes<V> ? fmaf(dh, br.rp, bl.lam[j]) : bl.lam[j];
         acc.k[j] = fmaf(dh, y, acc.k[j]);
         acc.xi[j] -= r;
         acc.z[j] = fmaf(-r, tt, acc.z[j]);
-        acc.a = fmaf(bl.lam[j], st.v[k][j], acc.a);
+        if constexpr (!kSL<V>) acc.a = fmaf(bl.lam[j], st.v[k][j], acc.a);
       } else {
         // u = ||d|| rz with d = Vd - xi over the branch's compartments;
         // du/dVd_i = rz d_i / ||d|| (0 at ||d|| = 0), du/dzeta = -u rz.
@@ -1057,10 +1061,10 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
 #pragma unroll
         for (int i = j * KC; i < (j + 1) * KC; ++i) {
           const float r = w * (st.v[k + 1][i] - br.xi[i]);
-          bl.lam[i] = fmaf(alpha, bl.lam[i], r);
+          bl.lam[i] = kSL<V> ? r : fmaf(alpha, bl.lam[i], r);
           gxo[i] = kRes<V> ? fmaf(dh, br.rp, bl.lam[i]) : bl.lam[i];
           acc.xi[i] -= r;
-          acc.a = fmaf(bl.lam[i], st.v[k][i], acc.a);
+          if constexpr (!kSL<V>) acc.a = fmaf(bl.lam[i], st.v[k][i], acc.a);
         }
         acc.k[j] = fmaf(dh, y, acc.k[j]);
         acc.z[j] = fmaf(-dhk, gzu, acc.z[j]);     // -kappa* dH psi'(u) u / zeta
@@ -1143,7 +1147,7 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
     const int t0 = seg * K;
     const int t1 = min(T, t0 + K);
     SegStart<E> ss;
-    load_seg_start<IO, E>(ba, lo, n0, seg, ss);
+    load_seg_start<IO, E, kSL<V>>(ba, lo, n0, seg, ss);
     // Chunks: the remainder (len mod KS) first, in descending powers of two
     // from t0, then whole KS-step chunks; visited from the last one back.  A
     // chunk re-runs the forward from t0 up to its first step, so putting the

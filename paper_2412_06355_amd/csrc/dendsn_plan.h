@@ -64,16 +64,20 @@ struct ScanArgs {
   int64_t ntiles;
 };
 
+// Checkpoints (when nck > 0): [nck][N][P] dendritic states (the stateful
+// dendrite only) followed by [nck][N] somatic potentials.
 struct FwdArgs {
   ScanArgs s;
   void* spikes;
   float* vsoma;  // optional
-  float* ckpt;   // optional; [nck][N][B] dendritic state then [nck][N] somatic potential
+  float* ckpt;   // [nck][N][P] dendritic states, or NULL (none kept, or the Stateless Dendrite)
+  float* ckh;    // [nck][N] somatic potentials, or NULL (none kept)
 };
 
 struct BwdArgs {
   ScanArgs s;
-  const float* ckpt;
+  const float* ckpt;  // as FwdArgs
+  const float* ckh;
   const void* gspk;
   const float* gv;  // optional
   void* gx;
@@ -103,6 +107,11 @@ struct FinArgs {
 };
 
 constexpr int kNarrowSlots = 16;  // up to this many partial slots: one thread per output
+
+// Runtime kernel variant v = psi | residual << 1 | stateless << 2, as the host
+// passes it to the launchers, to the template variant bits (bits 0, 1, 6).
+constexpr int variant_bits(int v) { return (v & 3) | ((v & 4) << 4); }
+#define DENDSN_EACH_VARIANT(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7)
 
 // Compiled (BL, L) mappings with one compartment per branch.  "Fast" mappings
 // move 8 or 16 bytes per lane; "generic" ones cover other branch counts.  For

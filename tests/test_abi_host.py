@@ -85,6 +85,9 @@ def test_ckpt_bytes(lib, T, K, batch, C, S, B, k):
     cfg = dendsn.DendSNConfig(T=T, batch=batch, C=C, S=S, B=B, ckpt_every=K, comps_per_branch=k)
     nck = -(-T // K) - 1
     assert dendsn.dendsn_ckpt_bytes(cfg) == nck * batch * C * S * (B * k + 1) * 4
+    # the Stateless Dendrite keeps only the somatic potential (its compartment
+    # state is the step's input)
+    assert dendsn.dendsn_ckpt_bytes(cfg.with_(stateful=False)) == nck * batch * C * S * 4
 
 
 def test_workspace_bytes_positive_and_grows_with_groups(lib):

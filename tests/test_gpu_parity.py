@@ -365,6 +365,57 @@ def test_checkpoint_interval_is_bit_invariant(gpu_device):
         assert torch.equal(_bits(o["grads"]["grad_x"]), _bits(ref["grads"]["grad_x"]))
 
 
+@pytest.mark.parametrize("shape", ["generic-kc2-S40", "fast-kc1-fc", "bf16-kc2-S300"])
+def test_stateless_checkpoint_interval_is_bit_invariant(gpu_device, shape):
+    """The Stateless Dendrite checkpoints only the somatic potential; its backward
+    restarts every segment from the input itself.  Every interval gives the
+    same bits (and matches the oracle)."""
+    import torch
+
+    kw = {"generic-kc2-S40": dict(T=10, batch=2, C=24, S=40, B=5, comps_per_branch=2),
+          "fast-kc1-fc": dict(T=13, batch=3, C=70, S=1, B=8),
+          "bf16-kc2-S300": dict(T=9, batch=2, C=8, S=300, B=4, comps_per_branch=2, io="bf16")}[shape]
+    base = cfg(stateful=False, beta=0.9, ckpt_every=4, **kw)
+    case = make_case(base, seed=19, x_mean=0.1, mask_rho=0.7, with_gv=True, name=f"stateless-ckpt/{shape}")
+    d = to_device(case, gpu_device)
+    outs = []
+    for K in (4, base.T, 3, 1):
+        case.cfg = base.with_(ckpt_every=K)
+        announce(f"stateless ckpt interval K={K}")
+        outs.append(run_gpu(case, gpu_device, dev=d)["raw"])
+    for o in outs[1:]:
+        assert torch.equal(o["spikes"], outs[0]["spikes"])
+        assert torch.equal(o["v_soma"], outs[0]["v_soma"])
+        for k in o["grads"]:
+            assert torch.equal(_bits(o["grads"][k]), _bits(outs[0]["grads"][k])), k
+    compare(case, run_gpu(case, gpu_device, dev=d))
+
+
+@pytest.mark.parametrize("shape", ["generic-kc2", "fast-kc1", "fast-kc2-bf16", "channel-major"])
+def test_stateless_equals_stateful_with_zero_alpha(gpu_device, shape):
+    """Methods, "DendSN variants": the Stateless Dendrite is the leaky one with
+    alpha = 0.  The stateless kernels (which drop the leak altogether) and the
+    stateful ones at alpha = 0 give equal spikes, potentials and gradients; only
+    g_alpha differs (the stateless layer has no alpha)."""
+    import torch
+
+    kw = {"generic-kc2": dict(T=10, batch=2, C=24, S=40, B=5, comps_per_branch=2, ckpt_every=4),
+          "fast-kc1": dict(T=4, batch=2, C=16, S=512, B=8),
+          "fast-kc2-bf16": dict(T=6, batch=2, C=8, S=300, B=4, comps_per_branch=2, io="bf16", ckpt_every=3),
+          "channel-major": dict(T=4, batch=2, C=16, S=100, B=2, comps_per_branch=2, layout="channel_major")}[shape]
+    base = cfg(stateful=False, beta=0.8, **kw)
+    case = make_case(base, seed=29, alpha=0.0, mask_rho=0.6, name=f"stateless-vs-alpha0/{shape}")
+    d = to_device(case, gpu_device)
+    a = run_gpu(case, gpu_device, dev=d)
+    case.cfg = base.with_(stateful=True)
+    b = run_gpu(case, gpu_device, dev=d)
+    assert torch.equal(a["raw"]["spikes"], b["raw"]["spikes"])
+    assert torch.equal(a["raw"]["v_soma"], b["raw"]["v_soma"])
+    for k in ("grad_x", "grad_kappa", "grad_xi", "grad_zeta", "grad_beta"):
+        assert torch.equal(a["raw"]["grads"][k], b["raw"]["grads"][k]), k
+    assert a["g_alpha"] == 0.0
+
+
 @pytest.mark.parametrize("B,io", [(8, "bf16"), (16, "bf16"), (64, "bf16"), (16, "f32")])
 def test_recompute_from_checkpoints_is_bit_exact(gpu_device, B, io):
     """The backward recomputes the forward from state checkpoints; it must reproduce
