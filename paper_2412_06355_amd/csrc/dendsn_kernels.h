@@ -306,10 +306,17 @@ __device__ __forceinline__ float load_row_one(const IO* row, uint32_t off) {
 template <typename IO, int E, bool CM>
 constexpr int kRawW = (sizeof(IO) == 2 && !CM && E % 2 == 0) ? E / 2 : E;  // dwords per row
 
-// Global (address) loads, as the forward issues them.
+// Global (address) loads, as the forward issues them (non-temporal, except for
+// lane rows of more than 16 bytes, as in bload_raw).
+template <typename T>
+__device__ __forceinline__ T stream_load(const T* p, bool cached) {
+  return cached ? *p : __builtin_nontemporal_load(p);
+}
+
 template <typename IO, int E, bool CM, int W>
 __device__ __forceinline__ void load_raw(const IO* row, uint32_t off, uint32_t es, uint32_t (&w)[W]) {
   constexpr bool dwords = sizeof(IO) == 4 || (!CM && W * 2 == E);  // contiguous whole dwords
+  constexpr bool wide = !CM && W * 4 > 16;
   if constexpr (CM) {
 #pragma unroll
     for (int i = 0; i < W; ++i) {
@@ -321,31 +328,35 @@ __device__ __forceinline__ void load_raw(const IO* row, uint32_t off, uint32_t e
     const u32x4_t* q = reinterpret_cast<const u32x4_t*>(at(row, off));
 #pragma unroll
     for (int i = 0; i < W / 4; ++i) {
-      const u32x4_t v = __builtin_nontemporal_load(q + i);
+      const u32x4_t v = stream_load(q + i, wide);
       w[4 * i] = v.x; w[4 * i + 1] = v.y; w[4 * i + 2] = v.z; w[4 * i + 3] = v.w;
     }
   } else if constexpr (dwords && W % 2 == 0) {
     const u32x2_t* q = reinterpret_cast<const u32x2_t*>(at(row, off));
 #pragma unroll
     for (int i = 0; i < W / 2; ++i) {
-      const u32x2_t v = __builtin_nontemporal_load(q + i);
+      const u32x2_t v = stream_load(q + i, wide);
       w[2 * i] = v.x; w[2 * i + 1] = v.y;
     }
   } else if constexpr (dwords) {
     const uint32_t* q = reinterpret_cast<const uint32_t*>(at(row, off));
 #pragma unroll
-    for (int i = 0; i < W; ++i) w[i] = __builtin_nontemporal_load(q + i);
+    for (int i = 0; i < W; ++i) w[i] = stream_load(q + i, wide);
   } else {
     const uint16_t* q = reinterpret_cast<const uint16_t*>(at(row, off));
 #pragma unroll
-    for (int i = 0; i < W; ++i) w[i] = uint32_t(__builtin_nontemporal_load(q + i));
+    for (int i = 0; i < W; ++i) w[i] = uint32_t(stream_load(q + i, wide));
   }
 }
 
-// Buffer loads, as the backward issues them.
+// Buffer loads, as the backward issues them.  A lane row of more than 16 bytes
+// takes several loads that each touch every cache line of the wave's row; those
+// go through the caches with the default policy, so the later loads of a row
+// find the lines the first one brought in.
 template <typename IO, int E, bool CM, int W>
 __device__ __forceinline__ void bload_raw(rsrc_t r, uint32_t off, uint32_t es, uint32_t (&w)[W]) {
   constexpr bool dwords = sizeof(IO) == 4 || (!CM && W * 2 == E);  // contiguous whole dwords
+  constexpr int kAuxNT = (!CM && W * 4 > 16) ? 0 : dendsn::kAuxNT;
   if constexpr (CM) {
 #pragma unroll
     for (int i = 0; i < W; ++i)
@@ -996,18 +1007,21 @@ __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branche
 }
 
 // The adjoint recurrences through one chunk, last step first; writes grad_x
-// and accumulates the parameter gradients.
-template <typename IO, int BL, int L, int V, int CS>
+// and accumulates the parameter gradients.  PART: only the first cs steps of
+// the chunk are real (cs is wave-uniform; the others are padding and skipped).
+template <typename IO, int BL, int L, int V, int CS, bool PART = false>
 __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, float beta_r, int c0, const Stash<BL, CS, V>& st,
                                               const float (&gs)[CS], const float (&gvr)[CS],
-                                              BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
+                                              BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc,
+                                              int cs = CS) {
   constexpr int KC = kKC<V>, E = BL * KC;
   const ScanArgs& a = ba.s;
   const int64_t rowX = a.N * a.P;
   const float beta = a.beta, vth = a.vth;
 #pragma unroll
   for (int k = CS - 1; k >= 0; --k) {
+    if (PART && k >= cs) continue;
     const float hk = st.h[k];
     const bool sk = hk >= vth;
     const float sgv = surrogate(hk - vth, kSG<V>, ba.sg_scale);
@@ -1242,6 +1256,118 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   item(cur, false, cur);
 }
 
+// The Stateless Dendrite over several checkpoint segments of at most KS steps
+// (K <= KS < T).  Its compartments carry no state from step to step, so a
+// segment restarts from its checkpointed somatic potential and its own inputs,
+// and nothing but dH crosses a segment boundary (in reverse time, within one
+// neuron).  Every (neuron, segment) visit is one chunk of KS rows, the rows past
+// the segment's end padding (they read one cache line of the segment's first
+// row per wave, compute, and are skipped by the adjoint pass).  Software-
+// pipelined over the lane's visits like single_chunk_items: the next visit's
+// rows and checkpoint are requested right after this visit's recompute, so they
+// stream in while its adjoint pass runs.  Visit order: batch items, the lane's
+// positions of each item, and each neuron's segments from last to first.
+template <typename IO, int E, int CS, bool CM>
+struct SegRaw {
+  ChunkRaw<IO, E, CS, CM> in;
+  float h0;  // somatic potential before the segment (0 for the first)
+};
+
+template <typename IO, int BL, int L, int V, int KS>
+__device__ __forceinline__ void load_segment_raw(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int64_t nx0,
+                                                 int seg, SegRaw<IO, BL * kKC<V>, KS, kCM<V>>& r) {
+  constexpr int E = BL * kKC<V>;
+  const ScanArgs& a = ba.s;
+  const int64_t rowX = a.N * a.P;
+  const int T = int(a.T), K = a.K;
+  const int c0 = seg * K;
+  const int len = min(K, T - c0);
+  const IO* x = static_cast<const IO*>(a.x) + nx0;
+  const IO* g = static_cast<const IO*>(ba.gspk) + n0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const bool real = k < len;
+    const int t = real ? c0 + k : c0;
+    bload_raw<IO, E, kCM<V>>(make_rsrc(x + int64_t(t) * rowX), real ? lo.x : 0u, a.xes, r.in.x[k]);
+    const rsrc_t rg = make_rsrc(g + int64_t(t) * a.N);
+    const uint32_t os = real ? lo.s : 0u;
+    r.in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, os, 0, kAuxNT)
+                                 : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, os, 0, kAuxNT));
+    r.in.gv[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, real ? ba.gvn : 0u), lo.v, 0, kAuxNT));
+  }
+  // checkpointed H after step c0 - 1 (a buffer of no bytes for the first segment)
+  const float* hp = seg > 0 ? ba.ckh + int64_t(seg - 1) * a.N + n0 : ba.gvz;
+  r.h0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(hp, seg > 0 ? 0xFFFFFFFFu : 0u), lo.v, 0,
+                                                                kAuxNT));
+}
+
+template <typename IO, int BL, int L, int V, int KS>
+__device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const LaneOff& lo,
+                                                        const Branches<BL, kKC<V>>& br, int64_t bt0, int nk,
+                                                        Accum<BL, BL * kKC<V>>& acc) {
+  constexpr int E = BL * kKC<V>;
+  const ScanArgs& a = ba.s;
+  const float beta_r = ba.detach ? 0.0f : a.beta;
+  const int T = int(a.T), K = a.K;
+  const int nseg = (T + K - 1) / K;
+  const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
+  const int nvis = wk.nw * nk * nseg;
+  if (nvis <= 0) return;
+  // two cursors over the same visit sequence: the visit being loaded, and the
+  // one being computed (wave-uniform)
+  struct Cursor {
+    int64_t n0, nx0;
+    int seg, w;
+  };
+  auto next = [&](Cursor& c) {
+    if (c.seg > 0) { --c.seg; return; }
+    c.seg = nseg - 1;
+    const bool last_w = ++c.w == wk.nw;
+    if (last_w) c.w = 0;
+    c.n0 += last_w ? wk.dn_item : wk.dn;
+    c.nx0 += last_w ? wk.dnx_item : wk.dnx;
+  };
+  Cursor ld{bt0 * a.M, bt0 * a.M * a.P, nseg - 1, 0};
+  Cursor cp = ld;
+  SegRaw<IO, E, KS, kCM<V>> cur;
+  load_segment_raw<IO, BL, L, V, KS>(ba, lo, ld.n0, ld.nx0, ld.seg, cur);
+  next(ld);
+  // Every later wait is then counted from loads issued inside the loop, whose
+  // next-visit loads are unconditional (the last visit runs after it).
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+  BwdLane<IO, E> bl;
+  bl.dh_next = 0.0f;
+  auto visit = [&](const SegRaw<IO, E, KS, kCM<V>>& in, bool more, SegRaw<IO, E, KS, kCM<V>>& nxt) {
+    const int c0 = cp.seg * K;
+    const int len = min(K, T - c0);
+    bl.gxbase = static_cast<IO*>(ba.gx) + cp.nx0;
+    if (cp.seg == nseg - 1) bl.dh_next = 0.0f;  // the neuron's last segment: nothing after it
+    float xin[KS][E], gsv[KS], zero[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) zero[j] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      raw_to_float<IO, E>(in.in.x[k], xin[k]);
+      gsv[k] = raw_to_float<IO>(in.in.gs[k]);
+    }
+    Stash<BL, KS, V> st;
+    recompute_chunk<BL, L, V, KS>(a, br, 0.0f, zero, in.h0, cp.seg > 0 && in.h0 >= a.vth, xin, st);
+    if (more) {
+      load_segment_raw<IO, BL, L, V, KS>(ba, lo, ld.n0, ld.nx0, ld.seg, nxt);
+      next(ld);
+    }
+    reverse_chunk<IO, BL, L, V, KS, true>(ba, lo, br, 0.0f, beta_r, c0, st, gsv, in.in.gv, bl, acc, len);
+    next(cp);
+  };
+  for (int i = 0; i + 1 < nvis; ++i) {
+    SegRaw<IO, E, KS, kCM<V>> nxt;
+    visit(cur, true, nxt);
+    cur = nxt;
+  }
+  visit(cur, false, cur);
+}
+
 // Per channel the backward produces W = 2 B + P parameter gradients, in the
 // order g_kappa [B], g_xi [P], g_zeta [B].  Partial slot p of output o of
 // channel c lives output-major ([C W][slots], read by one wave per output) when
@@ -1381,6 +1507,12 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     if constexpr (KS == 4) {
       if (T == KS) {
         single_chunk_items<IO, BL, L, V, KS>(ba, lo, br, alpha, bt0, nk, acc);
+        single = true;
+      }
+    }
+    if constexpr (kSL<V>) {
+      if (!single && a.K <= KS) {
+        stateless_segment_items<IO, BL, L, V, KS>(ba, lo, br, bt0, nk, acc);
         single = true;
       }
     }
