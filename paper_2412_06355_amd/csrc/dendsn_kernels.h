@@ -812,6 +812,120 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Forward fast path: T a multiple of D (no padding steps), no v_soma output and
+// checkpoints, if any, only at chunk ends (K a multiple of D; the kernel takes
+// it without interior checkpoints).  A step's bookkeeping is then the spike
+// store alone: a row's address is the previous row's plus one row stride, and
+// the checkpoint and next-neuron decisions are taken once per chunk.  A SIMD issues at most one scalar instruction per
+// vector instruction slot, so the general path's per-step address arithmetic
+// and conditions (more scalar than vector instructions per step) held the
+// kernel back.
+// ---------------------------------------------------------------------------
+template <typename IO, int BL, int L, int V, int D>
+__device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
+                                         float alpha, bool lead, int64_t bt0, int nk, const Walk& wk) {
+  constexpr int E = BL * kKC<V>;
+  constexpr int W = kRawW<IO, E, kCM<V>>;
+  const ScanArgs& a = fa.s;
+  const int T = int(a.T), K = a.K;
+  const int64_t rowX = a.N * a.P;
+  const int nchunks = nk * wk.nw * (T / D);
+  if (nchunks <= 0) return;
+  // load cursor (wave-uniform): the next chunk's first row, the row 0 of that
+  // chunk's neuron, its step and position index
+  const IO* lrow = static_cast<const IO*>(a.x) + bt0 * a.M * a.P;
+  const IO* lbase = lrow;
+  int lt = 0, lw = 0;
+  auto load = [&](uint32_t (&buf)[D][W]) {
+    const IO* r = lrow;
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      load_raw<IO, E, kCM<V>>(r, lo.x, a.xes, buf[k]);
+      r += rowX;
+    }
+    lt += D;
+    if (lt == T) {
+      lt = 0;
+      const bool last = ++lw == wk.nw;
+      if (last) lw = 0;
+      lbase += last ? wk.dnx_item : wk.dnx;
+      r = lbase;
+    }
+    lrow = r;
+  };
+  // the neuron being computed: state, step, position, output rows (uniform)
+  IO* const spk = static_cast<IO*>(fa.spikes);
+  int64_t n0 = bt0 * a.M;
+  IO* sp = spk + n0;
+  float* ckv = fa.ckpt ? fa.ckpt + n0 * a.P : nullptr;
+  float* ckh = fa.ckh ? fa.ckh + n0 : nullptr;
+  float vd[E];
+#pragma unroll
+  for (int j = 0; j < E; ++j) vd[j] = 0.0f;
+  float h = 0.0f;
+  bool s = false;
+  int ct = 0, cw = 0, kc = K;
+  auto compute = [&](const uint32_t (&buf)[D][W]) {
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      float xk[E];
+      if constexpr (kGateIn<IO, V>) raw_to_float_gated(buf[k], br.xsel, xk);
+      else raw_to_float<IO, E>(buf[k], xk);
+      const float z = dendrite_step<BL, L, V, kGateIn<IO, V>>(vd, xk, br, alpha);
+      soma_step(h, s, z, a.beta, a.vth);
+      if (lead) store_spike(at(sp, lo.s), s);
+      sp += a.N;
+    }
+    ct += D;
+    kc -= D;
+    if (kc == 0) {  // a checkpoint after this chunk's last step (none after the last step)
+      kc = K;
+      if (ckh && ct < T) {
+        if constexpr (!kSL<V>) {
+          store_vec<E>(at(ckv, lo.c), vd);
+          ckv += a.N * a.P;
+        }
+        if (lead) *at(ckh, lo.v) = h;
+        ckh += a.N;
+      }
+    }
+    if (ct == T) {  // next neuron of this lane: next position of the item, or the next item
+      ct = 0;
+      kc = K;
+      const bool last = ++cw == wk.nw;
+      if (last) cw = 0;
+      n0 += last ? wk.dn_item : wk.dn;
+      sp = spk + n0;
+      ckv = fa.ckpt ? fa.ckpt + n0 * a.P : nullptr;
+      ckh = fa.ckh ? fa.ckh + n0 : nullptr;
+#pragma unroll
+      for (int j = 0; j < E; ++j) vd[j] = 0.0f;
+      h = 0.0f;
+      s = false;
+    }
+  };
+  uint32_t bufA[D][W], bufB[D][W];
+  load(bufA);
+  // Every later wait is then counted from loads issued inside the loop, which
+  // are unconditional (the last one or two chunks run after it).
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+  int c = 0;
+  for (; c + 2 < nchunks; c += 2) {
+    load(bufB);
+    compute(bufA);
+    load(bufA);
+    compute(bufB);
+  }
+  if (c + 1 < nchunks) {
+    load(bufB);
+    compute(bufA);
+    compute(bufB);
+  } else {
+    compute(bufA);
+  }
+}
+
 template <typename IO, int BL, int L, int V>
 __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   constexpr int D = 4;  // rows per chunk; two chunks in flight per lane
@@ -831,6 +945,12 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   int64_t bt0;
   const int nk = items_of(a, pos, &bt0);
   const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
+  // (with interior checkpoints, e.g. the T = 64 layer with K = 8, the general
+  // path measured 2 % faster: those long sequences are bound by memory latency)
+  if (T % D == 0 && !fa.vsoma && a.nck == 0) {
+    fwd_fast<IO, BL, L, V, D>(fa, lo, br, alpha, lead, bt0, nk, wk);
+    return;
+  }
   const int nchunks = nk * wk.nw * (Tp / D);
 
   RowCursor<IO, E, D> cur;

@@ -153,6 +153,14 @@ def run_gpu(case: Case, device, dev=None, want_v_soma=True):
     d = dev if dev is not None else to_device(case, device)
     spikes, v_soma, ckpt = dendsn.forward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"],
                                           d["mask"], beta=d["beta"], want_v_soma=want_v_soma)
+    if want_v_soma:
+        # the forward without v_soma (as the benchmark runs it) takes the kernel's
+        # other path where one applies: the same spikes and checkpoints, bit for bit
+        s2, _, ck2 = dendsn.forward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"],
+                                    beta=d["beta"], want_v_soma=False)
+        assert torch.equal(s2.view(torch.uint8), spikes.view(torch.uint8)), "spikes differ without v_soma"
+        if ckpt is not None:
+            assert torch.equal(ck2.view(torch.uint8), ckpt.view(torch.uint8)), "checkpoints differ without v_soma"
     g = dendsn.backward(case.cfg, d["x"], d["alpha"], d["kappa"], d["xi"], d["zeta"], d["mask"], ckpt,
                         d["gS"], d["gV"], beta=d["beta"])
     torch.cuda.synchronize(device)

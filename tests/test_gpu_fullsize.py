@@ -46,7 +46,14 @@ def _check_against_oracle(wl, cfg, X, gS, kappa, alpha, p, mask_np, xg_files, tm
 
     dev = X.device
     mask = torch.from_numpy(mask_np).to(dev) if mask_np is not None else None
-    spikes, v_soma, ckpt = dendsn.forward(cfg, X, alpha, kappa, None, None, mask, want_v_soma=True)
+    # the forward as bench.py runs it (no v_soma), then again with v_soma for the
+    # potential's comparison: the spikes and checkpoints agree bit for bit
+    spikes, _, ckpt = dendsn.forward(cfg, X, alpha, kappa, None, None, mask)
+    s2, v_soma, ck2 = dendsn.forward(cfg, X, alpha, kappa, None, None, mask, want_v_soma=True)
+    assert torch.equal(s2.view(torch.uint8), spikes.view(torch.uint8))
+    if ckpt is not None:
+        assert torch.equal(ck2.view(torch.uint8), ckpt.view(torch.uint8))
+    del s2, ck2
     g = dendsn.backward(cfg, X, alpha, kappa, None, None, mask, ckpt, gS)
     torch.cuda.synchronize(dev)
     files = dict(xg_files, S=_dump(spikes, tmp_path / "S.f32"), H=_dump(v_soma, tmp_path / "H.f32"),
