@@ -46,6 +46,14 @@ template <int V> constexpr bool kSL = (V & 64) != 0;
 // gated or not).  Measured: forward 2-2.5 % faster; the backward kept its
 // per-step select (there the change was neutral to 1.4 % slower).
 template <typename IO, int V> constexpr bool kGateIn = sizeof(IO) == 2 && !kRes<V>;
+// The branch sum takes a lane's branches in fused pairs (one multiply and one
+// fused multiply-add per pair) when a lane holds at least two.  Every split of
+// a neuron that the two directions and the two layouts use holds whole pairs in
+// a lane whenever one of them does, except with four compartments per branch
+// (the channel-major backward then holds one branch per lane, its forward two),
+// which keeps the plain tree: the branch sum stays one tree over the fused
+// leaves, and the directions and layouts agree bit for bit.
+template <int V, int BL> constexpr bool kFuse = BL >= 2 && kKC<V> < 4;
 
 // -(1/2) log2(e): exp(-u^2/2) = exp2(u^2 * kNegHalfLog2e)
 constexpr float kNegHalfLog2e = -0.721347520444481703680f;
@@ -545,12 +553,15 @@ __device__ __forceinline__ float branch_sumsq(const float* vd, const float* xi) 
 // soma.  A gated-off branch keeps a zero state (its input zeroed, or its state
 // reset every step), so nothing it receives can reach the soma or its gradients.
 // ---------------------------------------------------------------------------
-// kGated: xv is already 0 on gated-off branches (their state then stays +0 by
-// itself), so the per-step select is skipped.
+// kGated: no select needed, because xv is already 0 on gated-off branches
+// (their state then stays +0 by itself) or because every branch of the lane is
+// on.  tfac / yfac (one compartment per branch, Mexican hat) receive each
+// branch's signed (Vd - xi) / zeta and psi as rounded here, for the adjoint.
 template <int BL, int L, int V, bool kGated = false>
 __device__ __forceinline__ float dendrite_step(float (&vd)[BL * kKC<V>], const float (&xv)[BL * kKC<V>],
                                                const Branches<BL, kKC<V>>& br, float alpha,
-                                               float* efac = nullptr) {
+                                               float* efac = nullptr, float* tfac = nullptr,
+                                               float* yfac = nullptr) {
   constexpr int KC = kKC<V>;
   float part[BL];
 #pragma unroll
@@ -572,15 +583,29 @@ __device__ __forceinline__ float dendrite_step(float (&vd)[BL * kKC<V>], const f
       const float e = __builtin_amdgcn_exp2f(q * kNegHalfLog2e);
       if (efac) efac[j] = e;
       y = fmaf(-q, e, e);  // (1 - q) e
+      if (tfac) tfac[j] = tt;
+      if (yfac) yfac[j] = y;
     } else {
       y = KC == 1 ? fabsf(tt) : tt;
     }
-    float pj = br.k[j] * y;
+    // branch pairs (2i, 2i+1) of a lane enter the sum as one fused leaf
+    // kappa*_{2i+1} Y_{2i+1} + kappa*_{2i} Y_{2i}; an odd branch count folds left
+    float pj = (kFuse<V, BL> && (BL % 2 == 0 ? (j & 1) : j > 0)) ? fmaf(br.k[j], y, part[j > 0 ? j - 1 : 0]) : br.k[j] * y;
     if constexpr (kRes<V>) {
 #pragma unroll
       for (int i = j * KC; i < (j + 1) * KC; ++i) pj = fmaf(xv[i], br.rp, pj);  // every compartment feeds the residual
     }
     part[j] = pj;
+  }
+  if constexpr (kFuse<V, BL>) {
+    if constexpr (BL % 2 == 0) {
+      float leaf[BL / 2];
+#pragma unroll
+      for (int i = 0; i < BL / 2; ++i) leaf[i] = part[2 * i + 1];
+      return group_sum<L>(lane_sum<BL / 2>(leaf));
+    } else {
+      return group_sum<L>(part[BL - 1]);
+    }
   }
   return group_sum<L>(lane_sum<BL>(part));
 }
@@ -590,15 +615,18 @@ __device__ __forceinline__ void soma_step(float& h, bool& s, float z, float beta
   s = h >= vth;                   // Theta(H - v_th), Theta(0) = 1
 }
 
-// Surrogate derivative of Theta at x = H - v_th; kind is a compile-time
-// constant of each backward kernel (dendsn_sg).
-__device__ __forceinline__ float surrogate(float x, int kind, float a) {
-  if (kind == 1) {  // a sigma(a x) (1 - sigma(a x)) = a e / (1 + e)^2, e = exp(-|a x|)
-    const float e = __builtin_amdgcn_exp2f(-fabsf(a * x) * kLog2e);
+// Surrogate derivative of Theta at x = H - v_th, with a x log2(e) (or pi x)
+// formed in one fused multiply-add from H; kind is a compile-time constant of
+// each backward kernel (dendsn_sg).
+__device__ __forceinline__ float surrogate(float h, float vth, int kind, float a) {
+  if (kind == 1) {  // a sigma(a x) (1 - sigma(a x)) = a e / (1 + e)^2, e = exp(-|a x|), x = h - v_th
+    const float ac = a * kLog2e;
+    const float t = fmaf(h, ac, -ac * vth);  // a x log2(e)
+    const float e = __builtin_amdgcn_exp2f(-fabsf(t));
     const float d = 1.0f + e;
     return a * e * __builtin_amdgcn_rcpf(d * d);
   }
-  const float px = kPi * x;  // 1 / (1 + pi^2 x^2)
+  const float px = fmaf(h, kPi, -kPi * vth);  // pi x: 1 / (1 + pi^2 x^2)
   return __builtin_amdgcn_rcpf(fmaf(px, px, 1.0f));
 }
 
@@ -1055,7 +1083,7 @@ struct ChunkRaw {
   float gv[CS];
 };
 
-template <typename IO, int E, int CS, bool CM>
+template <typename IO, int E, int CS, bool CM, bool GV = true>
 __device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
                                                const IO* gsbase, const float* gvbase, uint32_t gvbytes,
                                                ChunkRaw<IO, E, CS, CM>& in) {
@@ -1067,10 +1095,13 @@ __device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff&
     in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, lo.s, 0, kAuxNT)
                                : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, lo.s, 0, kAuxNT));
   }
-  // grad_v_soma rows (a buffer of no bytes when absent: every load returns 0)
+  // grad_v_soma rows (a buffer of no bytes when absent: every load returns 0);
+  // GV = false: known absent, nothing is requested
 #pragma unroll
   for (int k = 0; k < CS; ++k)
-    in.gv[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(gvbase + int64_t(k) * a.N, gvbytes), lo.v, 0, kAuxNT));
+    in.gv[k] = GV ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(gvbase + int64_t(k) * a.N, gvbytes),
+                                                                       lo.v, 0, kAuxNT))
+                  : 0.0f;
 }
 
 // The checkpointed state a segment starts from.
@@ -1100,13 +1131,18 @@ template <int BL, int CS, int V>
 struct Stash {
   float v[CS + 1][BL * kKC<V>];
   float e[kMH<V> ? CS : 1][BL];
+  // one compartment per branch with the Mexican hat: the signed (Vd - xi) / zeta
+  // and psi of each step, as the recompute rounded them
+  float t[kMH<V> && kKC<V> == 1 ? CS : 1][BL];
+  float y[kMH<V> && kKC<V> == 1 ? CS : 1][BL];
   float h[CS];
   float hd0;  // (1 - S) H before the chunk's first step: the decayed term beta multiplies
 };
 
 // Re-runs the chunk's forward steps exactly as the forward kernel did (the same
-// inline step function, so the same bits).
-template <int BL, int L, int V, int CS>
+// inline step function, so the same bits).  NG: every branch of the lane is on
+// (no gate select; with every branch on the select is the identity).
+template <int BL, int L, int V, int CS, bool NG = false>
 __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branches<BL, kKC<V>>& br, float alpha,
                                                 const float (&v0)[BL * kKC<V>], float h0, bool s0,
                                                 const float (&x)[CS][BL * kKC<V>], Stash<BL, CS, V>& st) {
@@ -1120,7 +1156,9 @@ __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branche
   for (int k = 0; k < CS; ++k) {
 #pragma unroll
     for (int j = 0; j < E; ++j) st.v[k + 1][j] = st.v[k][j];
-    const float z = dendrite_step<BL, L, V>(st.v[k + 1], x[k], br, alpha, kMH<V> ? st.e[kMH<V> ? k : 0] : nullptr);
+    constexpr bool ty = kMH<V> && kKC<V> == 1;
+    const float z = dendrite_step<BL, L, V, NG>(st.v[k + 1], x[k], br, alpha, kMH<V> ? st.e[kMH<V> ? k : 0] : nullptr,
+                                            ty ? st.t[ty ? k : 0] : nullptr, ty ? st.y[ty ? k : 0] : nullptr);
     soma_step(h, s, z, a.beta, a.vth);
     st.h[k] = h;
   }
@@ -1144,7 +1182,7 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
     if (PART && k >= cs) continue;
     const float hk = st.h[k];
     const bool sk = hk >= vth;
-    const float sgv = surrogate(hk - vth, kSG<V>, ba.sg_scale);
+    const float sgv = surrogate(hk, vth, kSG<V>, ba.sg_scale);
     const float dS = fmaf(-beta_r * hk, bl.dh_next, gs[k]);  // beta_r = 0: reset detached
     float dh = fmaf(sgv, dS, gvr[k]);
     dh = sk ? dh : fmaf(beta, bl.dh_next, dh);
@@ -1155,14 +1193,13 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
 #pragma unroll
     for (int j = 0; j < BL; ++j) {
       if constexpr (KC == 1) {
-        const float tt = (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
+        const float tt = kMH<V> ? st.t[kMH<V> ? k : 0][j] : (st.v[k + 1][j] - br.xi[j]) * br.rz[j];
         const float dhk = dh * br.krz[j];
         float y, r;  // psi(u), and r = kappa* dH psi'(u) sgn(Vd - xi) / zeta
         if constexpr (kMH<V>) {
-          const float q = tt * tt;
-          const float e = st.e[kMH<V> ? k : 0][j];
-          y = fmaf(-q, e, e);                          // (1 - q) e, rounded as in the forward
-          r = dhk * (tt * fmaf(-3.0f, e, q * e));      // psi'(u) sgn = tt (q - 3) e
+          const float e = st.e[k][j];
+          y = st.y[k][j];
+          r = (tt * fmaf(2.0f, e, y)) * -dhk;          // psi'(u) sgn = tt (q - 3) e = -tt (y + 2 e)
         } else {
           y = fabsf(tt);
           r = tt > 0.0f ? dhk : (tt < 0.0f ? -dhk : 0.0f);
@@ -1319,10 +1356,11 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
 
 // The common short-sequence case: T == KS, so every neuron is one chunk that
 // starts from the zero state.  Software-pipelined over the lane's neurons: the
-// next neuron's rows are requested right after this neuron's recompute, when
-// the registers of its own rows are free again, so they stream in while the
-// adjoint pass runs.
-template <typename IO, int BL, int L, int V, int KS>
+// next neuron's rows are requested as soon as this neuron's rows are widened to
+// float, so they stream in during its recompute and adjoint pass.  FAST: no
+// branch of the wave is gated off (no gate select, see recompute_chunk) and no
+// grad_v_soma is given (no loads of it).
+template <typename IO, int BL, int L, int V, int KS, bool FAST = false>
 __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo,
                                                    const Branches<BL, kKC<V>>& br, float alpha, int64_t bt0,
                                                    int nk, Accum<BL, BL * kKC<V>>& acc) {
@@ -1337,7 +1375,7 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   const IO* g = static_cast<const IO*>(ba.gspk);
   if (nvis <= 0) return;
   ChunkRaw<IO, E, KS, kCM<V>> cur;
-  load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, cur);
+  load_chunk_raw<IO, E, KS, kCM<V>, !FAST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, cur);
   // Every later wait is then counted from loads issued inside the loop, whose
   // next-neuron loads are unconditional (the last neuron runs after it).
   __builtin_amdgcn_s_waitcnt(kWaitVmem);
@@ -1357,16 +1395,22 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
       raw_to_float<IO, E>(in.x[k], xin[k]);
       gsv[k] = raw_to_float<IO>(in.gs[k]);
     }
-    Stash<BL, KS, V> st;
-    recompute_chunk<BL, L, V, KS>(a, br, alpha, zero, 0.0f, false, xin, st);
+    float gvv[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) gvv[k] = FAST ? 0.0f : in.gv[k];
     if (more) {
       const bool last_w = ++w == wk.nw;
       if (last_w) w = 0;
       n0 += last_w ? wk.dn_item : wk.dn;
       nx0 += last_w ? wk.dnx_item : wk.dnx;
-      load_chunk_raw<IO, E, KS, kCM<V>>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
+      load_chunk_raw<IO, E, KS, kCM<V>, !FAST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
     }
-    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, in.gv, bl, acc);
+    // Keeps the requests at this point: left to itself the scheduler sank them
+    // below most of the recompute (bf16 layers' backward 2-6 % slower).
+    __builtin_amdgcn_sched_barrier(0);
+    Stash<BL, KS, V> st;
+    recompute_chunk<BL, L, V, KS, FAST>(a, br, alpha, zero, 0.0f, false, xin, st);
+    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, gvv, bl, acc);
   };
   for (int i = 0; i + 1 < nvis; ++i) {
     ChunkRaw<IO, E, KS, kCM<V>> nxt;
@@ -1626,7 +1670,17 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     bool single = false;
     if constexpr (KS == 4) {
       if (T == KS) {
-        single_chunk_items<IO, BL, L, V, KS>(ba, lo, br, alpha, bt0, nk, acc);
+        // Without a gated-off branch in the wave (no mask, or a channel whose
+        // branches are all on) and without grad_v_soma, the recompute runs
+        // without the per-step gate select and no grad_v_soma rows are
+        // requested (bf16 ImageNet-stem layer: 434 -> 396 VALU instructions per
+        // neuron; bf16 backward 1-2 % faster without the empty loads).  The
+        // vote is wave-uniform, so each wave runs one copy.
+        bool all_on = true;
+#pragma unroll
+        for (int j = 0; j < BL; ++j) all_on = all_on && br.on[j];
+        if (__all(all_on) && !ba.gv) single_chunk_items<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc);
+        else single_chunk_items<IO, BL, L, V, KS>(ba, lo, br, alpha, bt0, nk, acc);
         single = true;
       }
     }
