@@ -46,9 +46,10 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(digest: str, workload: str):
-    """HBM bytes per backward launch from the committed rocprofv3 counter summary
-    of this workload, or None when there is none or the kernels changed since."""
+def measured_traffic(digest: str, workload: str, key: str = "hbm_bytes_per_launch"):
+    """HBM bytes per backward launch (key "fwd_hbm_bytes_per_launch": per forward
+    launch) from the committed rocprofv3 counter summary of this workload, or None
+    when there is none or the kernels changed since."""
     path = pmc_summary_path(workload)
     if not os.path.exists(path):
         return None
@@ -61,7 +62,7 @@ def measured_traffic(digest: str, workload: str):
     if vals.get("kernel_src_sha256_16") != digest or vals.get("workload") != workload:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals[key])
     except (KeyError, ValueError):
         return None
 
@@ -289,6 +290,7 @@ def main():
                      "unflushed": {"ms_per_launch": bwd_ms_nf,
                                    "frac": bwd_bytes / (bwd_ms_nf * 1e-3) / 1e9 / HBM_PEAK_GBS}},
         "roofline_fwd": {"achieved": fwd_gbs, "frac": fwd_gbs / HBM_PEAK_GBS, "unit": "GB/s",
+                         "traffic": measured_traffic(digest, wl.name, "fwd_hbm_bytes_per_launch"),
                          "algorithmic_bytes_per_launch": fwd_bytes, "ms_per_launch": fwd_ms,
                          "unflushed": {"ms_per_launch": fwd_ms_nf,
                                        "frac": fwd_bytes / (fwd_ms_nf * 1e-3) / 1e9 / HBM_PEAK_GBS}},

@@ -114,7 +114,8 @@ def _check_against_oracle(wl, cfg, X, gS, kappa, alpha, p, mask_np, xg_files, tm
 # every benchmark layer (bench.py --workload W), in the launch configuration it
 # times; the gated layer with each of its tasks' masks
 @pytest.mark.parametrize("name", ["cifar", "imagenet_stem", "long_horizon", "dbg", "cifar_bf16", "cifar_p4b2",
-                                  "cifar_p4b2_cm", "cifar_cm", "tiny_imagenet_res", "dvs_p10b5"])
+                                  "cifar_p4b2_cm", "cifar_cm", "tiny_imagenet_res", "dvs_p10b5",
+                                  "dvs_p10b5_stateful"])
 def test_full_size_against_oracle(gpu_device, name, tmp_path):
     import torch
 

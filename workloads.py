@@ -107,6 +107,10 @@ WORKLOADS = {
     # A state checkpoint every 4 steps keeps the backward's re-advance short.
     "dvs_p10b5": Workload("dvs_p10b5", T=10, batch=16, C=128, S=32 * 32, B=5, comps_per_branch=2,
                           stateful=False, ckpt_every=4),
+    # The same layer with the stateful dendrite (leak alpha = 0.5): the paper's
+    # cost ordering of the dendrite variants on one shape.
+    "dvs_p10b5_stateful": Workload("dvs_p10b5_stateful", T=10, batch=16, C=128, S=32 * 32, B=5,
+                                   comps_per_branch=2, ckpt_every=4),
 }
 
 
