@@ -375,6 +375,7 @@ void fill_scan(const dendsn_cfg* c, const Plan& p, const void* x, const float* a
   s->beta = c->beta; s->vth = c->v_th;
   s->mode = p.mode; s->ways = p.ways; s->pb = p.pb; s->tpc = p.tpc; s->cpt = p.cpt; s->nw = p.nw;
   s->xk = p.xk;
+  s->stg = !p.cm && (s->M * s->P * (c->io == DENDSN_IO_BF16 ? 2 : 4)) % 16 == 0;
   s->bpg = p.bpg; s->ntiles = p.ntiles;
 }
 

@@ -300,6 +300,28 @@ __device__ __forceinline__ void store_gx(IO* row, uint32_t off, uint32_t es, con
   }
 }
 
+// grad_x of one step, staged (see load_pieces): the lane's raw dwords go to the
+// wave's LDS buffer and leave as whole 16-byte pieces, consecutive lanes on
+// consecutive pieces (non-temporal: whole lines).
+template <typename IO, int E>
+__device__ __forceinline__ void store_gx_staged(IO* row, uint32_t span, const float (&v)[E], uint32_t* stage) {
+  constexpr int W = sizeof(IO) == 4 ? E : E / 2;
+  static_assert(sizeof(IO) == 4 || E % 2 == 0, "staged bf16 rows hold element pairs");
+  const uint32_t lane = __lane_id();
+#pragma unroll
+  for (int j = 0; j < W; ++j)
+    stage[lane * W + j] = sizeof(IO) == 4 ? __float_as_uint(v[j]) : pack_bf16x2(v[2 * j], v[2 * j + 1 < E ? 2 * j + 1 : 0]);
+  __builtin_amdgcn_wave_barrier();
+  const rsrc_t r = make_rsrc(row);
+#pragma unroll
+  for (int i = 0; i < (64 * W + 255) / 256; ++i) {
+    const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
+    if (i < 64 * W / 256 || lane < (64 * W % 256) / 4)  // whole rounds, then the partial one
+      __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(stage + d), r, span + d * 4, 0, kAuxNT);
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
 template <typename IO>
 __device__ __forceinline__ float load_row_one(const IO* row, uint32_t off) {
   return bload_one(make_rsrc(row), off, 0, row);
@@ -427,6 +449,89 @@ __device__ __forceinline__ void raw_to_float_gated(const uint32_t (&w)[W], const
 template <typename IO>
 __device__ __forceinline__ float raw_to_float(uint32_t w) {
   return sizeof(IO) == 4 ? __uint_as_float(w) : bf16_lo(w);
+}
+
+// ---------------------------------------------------------------------------
+// Wide lane rows (more than 16 bytes of a row in one lane: the one-lane
+// mappings of neurons with many compartments), staged.  Loaded lane by lane,
+// each of a lane's several loads touches every cache line of the wave's
+// stretch (a copy of 40-byte lane pieces ran 4.6-4.9 TB/s on MI355X against 5.7
+// for 16-byte lanes, a read 5.9 against 6.3).  When the wave's 64 lanes hold one
+// contiguous, 16-byte aligned stretch of 64 W dwords (every lane active), the
+// wave moves the stretch as whole 16-byte pieces instead, consecutive lanes on
+// consecutive pieces, and hands each lane its W dwords through a per-wave LDS
+// buffer (ST = true below).
+// ---------------------------------------------------------------------------
+template <int W> constexpr int kPieces = (64 * W + 255) / 256;  // 16-byte pieces per lane
+// Rows staged: a lane's row is more than 16 contiguous bytes that it keeps as
+// whole dwords (fp32 elements or bf16 pairs; not the channel-major layout).
+template <typename IO, int E, bool CM>
+constexpr bool kWideRow = !CM && (sizeof(IO) == 4 || E % 2 == 0) && E * int(sizeof(IO)) > 16;
+// dwords a lane keeps of one row: its W dwords, or its pieces when staged
+template <int W, bool ST> constexpr int kSlotW = ST ? 4 * kPieces<W> : W;
+
+// The pieces of the wave's stretch at byte `span` of `row` (non-temporal:
+// whole lines); a piece past the stretch rereads the stretch's first.
+// Round i of a stretch of 64 W dwords: lane l moves dwords 4 (64 i + l) ..
+// + 3; every lane takes part in the first 64 W / 256 rounds, lanes below
+// kTailLanes in the last, partial one.
+template <int W> constexpr int kFullRounds = 64 * W / 256;
+template <int W> constexpr uint32_t kTailLanes = (64 * W % 256) / 4;
+template <int W>
+__device__ __forceinline__ bool in_stretch(int i, uint32_t lane) {
+  return i < kFullRounds<W> || lane < kTailLanes<W>;
+}
+
+template <typename IO, int W>
+__device__ __forceinline__ void load_pieces(const IO* row, uint32_t span, uint32_t (&w)[4 * kPieces<W>]) {
+  const uint32_t lane = __lane_id();
+#pragma unroll
+  for (int i = 0; i < kPieces<W>; ++i) {
+    const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
+    const u32x4_t q = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4_t*>(at(row, span + (in_stretch<W>(i, lane) ? d * 4 : 0u))));
+    w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+  }
+}
+
+// The same through a buffer resource (the backward's rows).
+template <int W>
+__device__ __forceinline__ void bload_pieces(rsrc_t r, uint32_t span, uint32_t (&w)[4 * kPieces<W>]) {
+  const uint32_t lane = __lane_id();
+#pragma unroll
+  for (int i = 0; i < kPieces<W>; ++i) {
+    const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
+    const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(r, span + (in_stretch<W>(i, lane) ? d * 4 : 0u), 0, kAuxNT);
+    w[4 * i] = q.x; w[4 * i + 1] = q.y; w[4 * i + 2] = q.z; w[4 * i + 3] = q.w;
+  }
+}
+
+// The lane's W dwords out of the wave's pieces, through the wave's LDS buffer
+// `stage` (64 W dwords).  LDS accesses of one wave complete in order.
+template <int W>
+__device__ __forceinline__ void pieces_to_lane(const uint32_t (&w)[4 * kPieces<W>], uint32_t* stage,
+                                               uint32_t (&out)[W]) {
+  const uint32_t lane = __lane_id();
+#pragma unroll
+  for (int i = 0; i < kPieces<W>; ++i) {
+    const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
+    if (in_stretch<W>(i, lane)) *reinterpret_cast<u32x4_t*>(stage + d) = u32x4_t{w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int j = 0; j < W; ++j) out[j] = stage[lane * W + j];
+  __builtin_amdgcn_wave_barrier();
+}
+
+// A row slot (kSlotW dwords) as the lane's W raw dwords.
+template <int W, bool ST>
+__device__ __forceinline__ void slot_to_lane(const uint32_t (&slot)[kSlotW<W, ST>], uint32_t* stage, uint32_t (&out)[W]) {
+  if constexpr (ST) {
+    pieces_to_lane<W>(slot, stage, out);
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; ++j) out[j] = slot[j];
+  }
 }
 
 __device__ __forceinline__ void store_spike(float* p, bool s) { *p = s ? 1.0f : 0.0f; }
@@ -687,6 +792,7 @@ struct LaneOff {
   uint32_t c;   // checkpointed dendritic state (fp32)
   uint32_t s;   // spikes / grad_spikes (I/O dtype)
   uint32_t v;   // fp32 per-neuron rows (v_soma, grad_v_soma, checkpointed H)
+  uint32_t xw;  // staged wide rows (see load_pieces): the wave's stretch in X / grad_x
 };
 
 template <typename IO, int E, bool CM>
@@ -744,17 +850,21 @@ struct RowCursor {  // wave-uniform position of the next chunk to load
   int w, t;         // position index inside the item (0 .. nw-1), first row of the chunk
 };
 
-template <bool CM, typename IO, int BL, int D>
+template <bool CM, bool ST, typename IO, int BL, int D>
 __device__ __forceinline__ void load_chunk(const ScanArgs& a, RowCursor<IO, BL, D>& cur, uint32_t ox, int T,
                                            int Tp, int64_t rowX, const Walk& wk,
-                                           uint32_t (&buf)[D][kRawW<IO, BL, CM>]) {
+                                           uint32_t (&buf)[D][kSlotW<kRawW<IO, BL, CM>, ST>]) {
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     // A padding step past T (its result is discarded): every lane reads the
-    // start of row T - 1, one cache line per wave instead of a whole row.
+    // start of row T - 1, one cache line per wave instead of a whole row
+    // (staged: the first stretch of the row).
     const int tk = cur.t + k;
     const int t = min(tk, T - 1);
-    load_raw<IO, BL, CM>(cur.base + int64_t(t) * rowX, tk < T ? ox : 0u, a.xes, buf[k]);
+    if constexpr (ST)
+      load_pieces<IO, kRawW<IO, BL, CM>>(cur.base + int64_t(t) * rowX, tk < T ? ox : 0u, buf[k]);
+    else
+      load_raw<IO, BL, CM>(cur.base + int64_t(t) * rowX, tk < T ? ox : 0u, a.xes, buf[k]);
   }
   cur.t += D;
   if (cur.t >= Tp) {
@@ -796,19 +906,22 @@ __device__ __forceinline__ void fwd_item_start(const FwdArgs& fa, int64_t n0, Fw
   st.s = false;
 }
 
-template <typename IO, int BL, int L, int V, int D>
+template <typename IO, int BL, int L, int V, int D, bool ST>
 __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, bool lead, int T, int Tp, const Walk& wk,
-                                              const uint32_t (&buf)[D][kRawW<IO, BL * kKC<V>, kCM<V>>],
-                                              FwdLane<IO, BL * kKC<V>>& st) {
+                                              const uint32_t (&buf)[D][kSlotW<kRawW<IO, BL * kKC<V>, kCM<V>>, ST>],
+                                              uint32_t* stage, FwdLane<IO, BL * kKC<V>>& st) {
   constexpr int E = BL * kKC<V>;
+  constexpr int W = kRawW<IO, E, kCM<V>>;
   const ScanArgs& a = fa.s;
 #pragma unroll
   for (int k = 0; k < D; ++k) {
     const int t = st.t + k;
     float xk[E];
-    if constexpr (kGateIn<IO, V>) raw_to_float_gated(buf[k], br.xsel, xk);
-    else raw_to_float<IO, E>(buf[k], xk);
+    uint32_t raw[W];
+    slot_to_lane<W, ST>(buf[k], stage, raw);
+    if constexpr (kGateIn<IO, V>) raw_to_float_gated(raw, br.xsel, xk);
+    else raw_to_float<IO, E>(raw, xk);
     const float z = dendrite_step<BL, L, V, kGateIn<IO, V>>(st.vd, xk, br, alpha);
     soma_step(st.h, st.s, z, a.beta, a.vth);
     if (t < T) {  // padded steps store nothing
@@ -850,11 +963,13 @@ __device__ __forceinline__ void compute_chunk(const FwdArgs& fa, const LaneOff& 
 // and conditions (more scalar than vector instructions per step) held the
 // kernel back.
 // ---------------------------------------------------------------------------
-template <typename IO, int BL, int L, int V, int D>
+template <typename IO, int BL, int L, int V, int D, bool ST>
 __device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
-                                         float alpha, bool lead, int64_t bt0, int nk, const Walk& wk) {
+                                         float alpha, bool lead, int64_t bt0, int nk, const Walk& wk,
+                                         uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
   constexpr int W = kRawW<IO, E, kCM<V>>;
+  constexpr int SW = kSlotW<W, ST>;
   const ScanArgs& a = fa.s;
   const int T = int(a.T), K = a.K;
   const int64_t rowX = a.N * a.P;
@@ -865,11 +980,12 @@ __device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, c
   const IO* lrow = static_cast<const IO*>(a.x) + bt0 * a.M * a.P;
   const IO* lbase = lrow;
   int lt = 0, lw = 0;
-  auto load = [&](uint32_t (&buf)[D][W]) {
+  auto load = [&](uint32_t (&buf)[D][SW]) {
     const IO* r = lrow;
 #pragma unroll
     for (int k = 0; k < D; ++k) {
-      load_raw<IO, E, kCM<V>>(r, lo.x, a.xes, buf[k]);
+      if constexpr (ST) load_pieces<IO, W>(r, lo.x, buf[k]);
+      else load_raw<IO, E, kCM<V>>(r, lo.x, a.xes, buf[k]);
       r += rowX;
     }
     lt += D;
@@ -894,12 +1010,14 @@ __device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, c
   float h = 0.0f;
   bool s = false;
   int ct = 0, cw = 0, kc = K;
-  auto compute = [&](const uint32_t (&buf)[D][W]) {
+  auto compute = [&](const uint32_t (&buf)[D][SW]) {
 #pragma unroll
     for (int k = 0; k < D; ++k) {
       float xk[E];
-      if constexpr (kGateIn<IO, V>) raw_to_float_gated(buf[k], br.xsel, xk);
-      else raw_to_float<IO, E>(buf[k], xk);
+      uint32_t raw[W];
+      slot_to_lane<W, ST>(buf[k], stage, raw);
+      if constexpr (kGateIn<IO, V>) raw_to_float_gated(raw, br.xsel, xk);
+      else raw_to_float<IO, E>(raw, xk);
       const float z = dendrite_step<BL, L, V, kGateIn<IO, V>>(vd, xk, br, alpha);
       soma_step(h, s, z, a.beta, a.vth);
       if (lead) store_spike(at(sp, lo.s), s);
@@ -933,7 +1051,7 @@ __device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, c
       s = false;
     }
   };
-  uint32_t bufA[D][W], bufB[D][W];
+  uint32_t bufA[D][SW], bufB[D][SW];
   load(bufA);
   // Every later wait is then counted from loads issued inside the loop, which
   // are unconditional (the last one or two chunks run after it).
@@ -954,29 +1072,22 @@ __device__ __forceinline__ void fwd_fast(const FwdArgs& fa, const LaneOff& lo, c
   }
 }
 
-template <typename IO, int BL, int L, int V>
-__global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
-  constexpr int D = 4;  // rows per chunk; two chunks in flight per lane
-  if (fa.s.beta_p) fa.s.beta = fa.s.beta_p[0];  // learnable (PLIF) decay
-  const ScanArgs& a = fa.s;
-  const Pos pos = locate<L>(a);
-  if (!pos.active) return;  // whole L-lane groups leave together
+// The forward of the lane's neurons (ST: wide rows staged, see load_pieces;
+// lo.x is then the wave's stretch, the same for every lane).
+template <typename IO, int BL, int L, int V, int D, bool ST>
+__device__ __forceinline__ void fwd_run(const FwdArgs& fa, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
+                                        float alpha, bool lead, int64_t bt0, int nk, uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
-  Branches<BL, kKC<V>> br;
-  load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br, kRawW<IO, E, kCM<V>> * 2 == E);
-  const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-  const LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
-  const bool lead = pos.sub == 0;
+  constexpr int SW = kSlotW<kRawW<IO, E, kCM<V>>, ST>;
+  const ScanArgs& a = fa.s;
   const int T = int(a.T);
   const int Tp = (T + D - 1) / D * D;
   const int64_t rowX = a.N * a.P;
-  int64_t bt0;
-  const int nk = items_of(a, pos, &bt0);
   const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
   // (with interior checkpoints, e.g. the T = 64 layer with K = 8, the general
   // path measured 2 % faster: those long sequences are bound by memory latency)
   if (T % D == 0 && !fa.vsoma && a.nck == 0) {
-    fwd_fast<IO, BL, L, V, D>(fa, lo, br, alpha, lead, bt0, nk, wk);
+    fwd_fast<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, bt0, nk, wk, stage);
     return;
   }
   const int nchunks = nk * wk.nw * (Tp / D);
@@ -990,25 +1101,65 @@ __global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
   fwd_item_start<IO, E>(fa, bt0 * a.M, st);
 
   if (nchunks <= 0) return;
-  uint32_t bufA[D][kRawW<IO, E, kCM<V>>], bufB[D][kRawW<IO, E, kCM<V>>];
-  load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
+  uint32_t bufA[D][SW], bufB[D][SW];
+  load_chunk<kCM<V>, ST>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
   // Every later wait is then counted from loads issued inside the loop, which
   // are unconditional (the last one or two chunks run after it).
   __builtin_amdgcn_s_waitcnt(kWaitVmem);
   int c = 0;
   for (; c + 2 < nchunks; c += 2) {
-    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
-    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
+    load_chunk<kCM<V>, ST>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
+    compute_chunk<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, stage, st);
+    load_chunk<kCM<V>, ST>(a, cur, lo.x, T, Tp, rowX, wk, bufA);
+    compute_chunk<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, stage, st);
   }
   if (c + 1 < nchunks) {
-    load_chunk<kCM<V>>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, st);
+    load_chunk<kCM<V>, ST>(a, cur, lo.x, T, Tp, rowX, wk, bufB);
+    compute_chunk<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, stage, st);
+    compute_chunk<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, T, Tp, wk, bufB, stage, st);
   } else {
-    compute_chunk<IO, BL, L, V, D>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, st);
+    compute_chunk<IO, BL, L, V, D, ST>(fa, lo, br, alpha, lead, T, Tp, wk, bufA, stage, st);
   }
+}
+
+// Whether a wave may stage its wide rows: every lane active (checked by the
+// caller), the layer's per-sample slice a multiple of 16 bytes (the host's
+// flag: then every row and item keeps the alignment of the first), and the
+// wave's first stretch 16-byte aligned.  lo.x of lane 0 is the stretch's start.
+template <typename IO>
+__device__ __forceinline__ bool stage_rows(const ScanArgs& a, uint32_t span0, int64_t bt0) {
+  const uintptr_t p = reinterpret_cast<uintptr_t>(static_cast<const IO*>(a.x) + bt0 * a.M * a.P) + span0;
+  return a.stg && (p & 15) == 0;
+}
+
+template <typename IO, int BL, int L, int V>
+__global__ void __launch_bounds__(kThreads) dendsn_fwd_kernel(FwdArgs fa) {
+  constexpr int D = 4;  // rows per chunk; two chunks in flight per lane
+  if (fa.s.beta_p) fa.s.beta = fa.s.beta_p[0];  // learnable (PLIF) decay
+  const ScanArgs& a = fa.s;
+  const Pos pos = locate<L>(a);
+  constexpr int E = BL * kKC<V>;
+  constexpr int W = kRawW<IO, E, kCM<V>>;
+  constexpr bool kWide = kWideRow<IO, E, kCM<V>>;
+  const bool full = kWide && __all(pos.active);
+  if (!pos.active) return;  // whole L-lane groups leave together
+  Branches<BL, kKC<V>> br;
+  load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br, W * 2 == E);
+  const float alpha = a.alpha ? a.alpha[0] : 0.0f;
+  LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
+  const bool lead = pos.sub == 0;
+  int64_t bt0;
+  const int nk = items_of(a, pos, &bt0);
+  if constexpr (kWide) {
+    __shared__ uint32_t stage[kThreads / 64][64 * W];
+    const uint32_t span = __builtin_amdgcn_readfirstlane(lo.x);
+    if (full && stage_rows<IO>(a, span, bt0)) {
+      lo.x = span;
+      fwd_run<IO, BL, L, V, D, true>(fa, lo, br, alpha, lead, bt0, nk, stage[threadIdx.x >> 6]);
+      return;
+    }
+  }
+  fwd_run<IO, BL, L, V, D, false>(fa, lo, br, alpha, lead, bt0, nk, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -1031,6 +1182,7 @@ template <typename IO, int E>
 struct BwdLane {  // adjoint state carried backwards through time, and pointers
   float dh_next;
   float lam[E];
+  uint32_t* stage;   // the wave's LDS buffer for staged wide rows (see load_pieces)
   const IO* xbase;   // X of this batch item (uniform)
   IO* gxbase;
   const IO* gsbase;
@@ -1076,21 +1228,22 @@ __device__ __forceinline__ void load_chunk_in(const ScanArgs& a, const LaneOff& 
 // carries the next neuron's rows this way: a conversion issued next to the
 // loads would make the wave wait for them at once instead of while the current
 // neuron's adjoint pass runs.
-template <typename IO, int E, int CS, bool CM>
+template <typename IO, int E, int CS, bool CM, bool ST = false>
 struct ChunkRaw {
-  uint32_t x[CS][kRawW<IO, E, CM>];
+  uint32_t x[CS][kSlotW<kRawW<IO, E, CM>, ST>];
   uint32_t gs[CS];
   float gv[CS];
 };
 
-template <typename IO, int E, int CS, bool CM, bool GV = true>
+template <typename IO, int E, int CS, bool CM, bool GV = true, bool ST = false>
 __device__ __forceinline__ void load_chunk_raw(const ScanArgs& a, const LaneOff& lo, const IO* xbase,
                                                const IO* gsbase, const float* gvbase, uint32_t gvbytes,
-                                               ChunkRaw<IO, E, CS, CM>& in) {
+                                               ChunkRaw<IO, E, CS, CM, ST>& in) {
   const int64_t rowX = a.N * a.P;
 #pragma unroll
   for (int k = 0; k < CS; ++k) {
-    bload_raw<IO, E, CM>(make_rsrc(xbase + k * rowX), lo.x, a.xes, in.x[k]);
+    if constexpr (ST) bload_pieces<kRawW<IO, E, CM>>(make_rsrc(xbase + k * rowX), lo.xw, in.x[k]);
+    else bload_raw<IO, E, CM>(make_rsrc(xbase + k * rowX), lo.x, a.xes, in.x[k]);
     const rsrc_t rg = make_rsrc(gsbase + k * a.N);
     in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, lo.s, 0, kAuxNT)
                                : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, lo.s, 0, kAuxNT));
@@ -1167,7 +1320,7 @@ __device__ __forceinline__ void recompute_chunk(const ScanArgs& a, const Branche
 // The adjoint recurrences through one chunk, last step first; writes grad_x
 // and accumulates the parameter gradients.  PART: only the first cs steps of
 // the chunk are real (cs is wave-uniform; the others are padding and skipped).
-template <typename IO, int BL, int L, int V, int CS, bool PART = false>
+template <typename IO, int BL, int L, int V, int CS, bool PART = false, bool ST = false>
 __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                               float alpha, float beta_r, int c0, const Stash<BL, CS, V>& st,
                                               const float (&gs)[CS], const float (&gvr)[CS],
@@ -1241,19 +1394,20 @@ __device__ __forceinline__ void reverse_chunk(const BwdArgs& ba, const LaneOff& 
         acc.z[j] = fmaf(-dhk, gzu, acc.z[j]);     // -kappa* dH psi'(u) u / zeta
       }
     }
-    store_gx<E, kCM<V>>(bl.gxbase + int64_t(c0 + k) * rowX, lo.x, a.xes, gxo);
+    if constexpr (ST) store_gx_staged<IO, E>(bl.gxbase + int64_t(c0 + k) * rowX, lo.xw, gxo, bl.stage);
+    else store_gx<E, kCM<V>>(bl.gxbase + int64_t(c0 + k) * rowX, lo.x, a.xes, gxo);
     bl.dh_next = dh;
   }
 }
 
-template <typename IO, int BL, int L, int V, int CS>
+template <typename IO, int BL, int L, int V, int CS, bool ST = false>
 __device__ __forceinline__ void bwd_chunk(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
                                           float alpha, float beta_r, int c0, const float (&v0)[BL * kKC<V>],
                                           float h0, bool s0, const ChunkIn<BL * kKC<V>, CS>& in,
                                           BwdLane<IO, BL * kKC<V>>& bl, Accum<BL, BL * kKC<V>>& acc) {
   Stash<BL, CS, V> st;
   recompute_chunk<BL, L, V, CS>(ba.s, br, alpha, v0, h0, s0, in.x, st);
-  reverse_chunk<IO, BL, L, V, CS>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
+  reverse_chunk<IO, BL, L, V, CS, false, ST>(ba, lo, br, alpha, beta_r, c0, st, in.gs, in.gv, bl, acc);
 }
 
 // Runs the forward from (vd, h, s) at step t_from up to (not including) t_to.
@@ -1272,7 +1426,7 @@ __device__ __forceinline__ void advance(const ScanArgs& a, const LaneOff& lo, co
 }
 
 // Loads a chunk of CS steps and runs it (used for every chunk but a prefetched one).
-template <typename IO, int BL, int L, int V, int CS>
+template <typename IO, int BL, int L, int V, int CS, bool ST = false>
 __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const LaneOff& lo,
                                                    const Branches<BL, kKC<V>>& br, float alpha, float beta_r,
                                                    int t0, int c0, const SegStart<BL * kKC<V>>& ss,
@@ -1286,7 +1440,7 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
   float h = ss.h;
   bool s = ss.h >= ba.s.vth && t0 > 0;
   advance<IO, BL, L, V>(ba.s, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-  bwd_chunk<IO, BL, L, V, CS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+  bwd_chunk<IO, BL, L, V, CS, ST>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
 }
 
 // Chunk plan of a segment [t0, t1): whole KS-step chunks from t0, then the
@@ -1294,10 +1448,10 @@ __device__ __forceinline__ void load_and_run_chunk(const BwdArgs& ba, const Lane
 // from the last step backwards.  A neuron's first visited chunk is the top of
 // its last segment; it is a full KS chunk exactly when that segment's length
 // is a multiple of KS, and only then is it prefetched.
-template <typename IO, int BL, int L, int V, int KS>
+template <typename IO, int BL, int L, int V, int KS, bool ST = false>
 __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff& lo, int64_t bt,
                                                 const Branches<BL, kKC<V>>& br, float alpha,
-                                                Accum<BL, BL * kKC<V>>& acc) {
+                                                Accum<BL, BL * kKC<V>>& acc, uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const int T = int(a.T);
@@ -1310,6 +1464,7 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
   bl.gsbase = static_cast<const IO*>(ba.gspk) + n0;
   bl.gvbase = ba.gv ? ba.gv + n0 : nullptr;
   bl.dh_next = 0.0f;
+  bl.stage = stage;
 #pragma unroll
   for (int j = 0; j < E; ++j) bl.lam[j] = 0.0f;
 
@@ -1336,7 +1491,7 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
       float h = ss.h;
       bool s = ss.h >= a.vth && t0 > 0;
       advance<IO, BL, L, V>(a, lo, br, alpha, bl.xbase, t0, c0, v, h, s);
-      bwd_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
+      bwd_chunk<IO, BL, L, V, KS, ST>(ba, lo, br, alpha, beta_r, c0, v, h, s, in, bl, acc);
     }
     // remainder pieces fill [t0, t0 + rem) with the largest on top and the
     // smallest at t0 (their re-advances then sum to the least); top one first
@@ -1345,9 +1500,9 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
     for (int cs = KS / 2; cs >= 1; cs /= 2) {
       if (rem & cs) {
         const int c0 = top - cs;
-        if (cs == 4) load_and_run_chunk<IO, BL, L, V, (KS >= 8 ? 4 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
-        else if (cs == 2) load_and_run_chunk<IO, BL, L, V, (KS >= 4 ? 2 : 1)>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
-        else load_and_run_chunk<IO, BL, L, V, 1>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        if (cs == 4) load_and_run_chunk<IO, BL, L, V, (KS >= 8 ? 4 : 1), ST>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else if (cs == 2) load_and_run_chunk<IO, BL, L, V, (KS >= 4 ? 2 : 1), ST>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
+        else load_and_run_chunk<IO, BL, L, V, 1, ST>(ba, lo, br, alpha, beta_r, t0, c0, ss, bl, acc);
         top = c0;
       }
     }
@@ -1360,10 +1515,10 @@ __device__ __forceinline__ void backward_neuron(const BwdArgs& ba, const LaneOff
 // float, so they stream in during its recompute and adjoint pass.  FAST: no
 // branch of the wave is gated off (no gate select, see recompute_chunk) and no
 // grad_v_soma is given (no loads of it).
-template <typename IO, int BL, int L, int V, int KS, bool FAST = false>
+template <typename IO, int BL, int L, int V, int KS, bool FAST = false, bool ST = false>
 __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const LaneOff& lo,
                                                    const Branches<BL, kKC<V>>& br, float alpha, int64_t bt0,
-                                                   int nk, Accum<BL, BL * kKC<V>>& acc) {
+                                                   int nk, Accum<BL, BL * kKC<V>>& acc, uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const float beta_r = ba.detach ? 0.0f : a.beta;
@@ -1374,14 +1529,16 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
   const IO* x = static_cast<const IO*>(a.x);
   const IO* g = static_cast<const IO*>(ba.gspk);
   if (nvis <= 0) return;
-  ChunkRaw<IO, E, KS, kCM<V>> cur;
-  load_chunk_raw<IO, E, KS, kCM<V>, !FAST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, cur);
+  constexpr int W = kRawW<IO, E, kCM<V>>;
+  ChunkRaw<IO, E, KS, kCM<V>, ST> cur;
+  load_chunk_raw<IO, E, KS, kCM<V>, !FAST, ST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, cur);
   // Every later wait is then counted from loads issued inside the loop, whose
   // next-neuron loads are unconditional (the last neuron runs after it).
   __builtin_amdgcn_s_waitcnt(kWaitVmem);
   int w = 0;
-  auto item = [&](const ChunkRaw<IO, E, KS, kCM<V>>& in, bool more, ChunkRaw<IO, E, KS, kCM<V>>& nxt) {
+  auto item = [&](const ChunkRaw<IO, E, KS, kCM<V>, ST>& in, bool more, ChunkRaw<IO, E, KS, kCM<V>, ST>& nxt) {
     BwdLane<IO, E> bl;
+    bl.stage = stage;
     bl.xbase = x + nx0;
     bl.gxbase = static_cast<IO*>(ba.gx) + nx0;
     bl.gsbase = g + n0;
@@ -1392,7 +1549,9 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
     for (int j = 0; j < E; ++j) { bl.lam[j] = 0.0f; zero[j] = 0.0f; }
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-      raw_to_float<IO, E>(in.x[k], xin[k]);
+      uint32_t raw[W];
+      slot_to_lane<W, ST>(in.x[k], stage, raw);
+      raw_to_float<IO, E>(raw, xin[k]);
       gsv[k] = raw_to_float<IO>(in.gs[k]);
     }
     float gvv[KS];
@@ -1403,17 +1562,17 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
       if (last_w) w = 0;
       n0 += last_w ? wk.dn_item : wk.dn;
       nx0 += last_w ? wk.dnx_item : wk.dnx;
-      load_chunk_raw<IO, E, KS, kCM<V>, !FAST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
+      load_chunk_raw<IO, E, KS, kCM<V>, !FAST, ST>(a, lo, x + nx0, g + n0, ba.gvz + n0, ba.gvn, nxt);
     }
     // Keeps the requests at this point: left to itself the scheduler sank them
     // below most of the recompute (bf16 layers' backward 2-6 % slower).
     __builtin_amdgcn_sched_barrier(0);
     Stash<BL, KS, V> st;
     recompute_chunk<BL, L, V, KS, FAST>(a, br, alpha, zero, 0.0f, false, xin, st);
-    reverse_chunk<IO, BL, L, V, KS>(ba, lo, br, alpha, beta_r, 0, st, gsv, gvv, bl, acc);
+    reverse_chunk<IO, BL, L, V, KS, false, ST>(ba, lo, br, alpha, beta_r, 0, st, gsv, gvv, bl, acc);
   };
   for (int i = 0; i + 1 < nvis; ++i) {
-    ChunkRaw<IO, E, KS, kCM<V>> nxt;
+    ChunkRaw<IO, E, KS, kCM<V>, ST> nxt;
     item(cur, true, nxt);
     cur = nxt;
   }
@@ -1431,15 +1590,15 @@ __device__ __forceinline__ void single_chunk_items(const BwdArgs& ba, const Lane
 // rows and checkpoint are requested right after this visit's recompute, so they
 // stream in while its adjoint pass runs.  Visit order: batch items, the lane's
 // positions of each item, and each neuron's segments from last to first.
-template <typename IO, int E, int CS, bool CM>
+template <typename IO, int E, int CS, bool CM, bool ST = false>
 struct SegRaw {
-  ChunkRaw<IO, E, CS, CM> in;
+  ChunkRaw<IO, E, CS, CM, ST> in;
   float h0;  // somatic potential before the segment (0 for the first)
 };
 
-template <typename IO, int BL, int L, int V, int KS>
+template <typename IO, int BL, int L, int V, int KS, bool GV = true, bool ST = false>
 __device__ __forceinline__ void load_segment_raw(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int64_t nx0,
-                                                 int seg, SegRaw<IO, BL * kKC<V>, KS, kCM<V>>& r) {
+                                                 int seg, SegRaw<IO, BL * kKC<V>, KS, kCM<V>, ST>& r) {
   constexpr int E = BL * kKC<V>;
   const ScanArgs& a = ba.s;
   const int64_t rowX = a.N * a.P;
@@ -1452,13 +1611,15 @@ __device__ __forceinline__ void load_segment_raw(const BwdArgs& ba, const LaneOf
   for (int k = 0; k < KS; ++k) {
     const bool real = k < len;
     const int t = real ? c0 + k : c0;
-    bload_raw<IO, E, kCM<V>>(make_rsrc(x + int64_t(t) * rowX), real ? lo.x : 0u, a.xes, r.in.x[k]);
+    if constexpr (ST) bload_pieces<kRawW<IO, E, kCM<V>>>(make_rsrc(x + int64_t(t) * rowX), real ? lo.xw : 0u, r.in.x[k]);
+    else bload_raw<IO, E, kCM<V>>(make_rsrc(x + int64_t(t) * rowX), real ? lo.x : 0u, a.xes, r.in.x[k]);
     const rsrc_t rg = make_rsrc(g + int64_t(t) * a.N);
     const uint32_t os = real ? lo.s : 0u;
     r.in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, os, 0, kAuxNT)
                                  : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, os, 0, kAuxNT));
-    r.in.gv[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-        make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, real ? ba.gvn : 0u), lo.v, 0, kAuxNT));
+    r.in.gv[k] = GV ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                          make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, real ? ba.gvn : 0u), lo.v, 0, kAuxNT))
+                    : 0.0f;  // GV = false: known absent, nothing is requested
   }
   // checkpointed H after step c0 - 1 (a buffer of no bytes for the first segment)
   const float* hp = seg > 0 ? ba.ckh + int64_t(seg - 1) * a.N + n0 : ba.gvz;
@@ -1466,11 +1627,12 @@ __device__ __forceinline__ void load_segment_raw(const BwdArgs& ba, const LaneOf
                                                                 kAuxNT));
 }
 
-template <typename IO, int BL, int L, int V, int KS>
+template <typename IO, int BL, int L, int V, int KS, bool FAST = false, bool ST = false>
 __device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const LaneOff& lo,
                                                         const Branches<BL, kKC<V>>& br, int64_t bt0, int nk,
-                                                        Accum<BL, BL * kKC<V>>& acc) {
+                                                        Accum<BL, BL * kKC<V>>& acc, uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
+  constexpr int W = kRawW<IO, E, kCM<V>>;
   const ScanArgs& a = ba.s;
   const float beta_r = ba.detach ? 0.0f : a.beta;
   const int T = int(a.T), K = a.K;
@@ -1494,15 +1656,16 @@ __device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const
   };
   Cursor ld{bt0 * a.M, bt0 * a.M * a.P, nseg - 1, 0};
   Cursor cp = ld;
-  SegRaw<IO, E, KS, kCM<V>> cur;
-  load_segment_raw<IO, BL, L, V, KS>(ba, lo, ld.n0, ld.nx0, ld.seg, cur);
+  SegRaw<IO, E, KS, kCM<V>, ST> cur;
+  load_segment_raw<IO, BL, L, V, KS, !FAST, ST>(ba, lo, ld.n0, ld.nx0, ld.seg, cur);
   next(ld);
   // Every later wait is then counted from loads issued inside the loop, whose
   // next-visit loads are unconditional (the last visit runs after it).
   __builtin_amdgcn_s_waitcnt(kWaitVmem);
   BwdLane<IO, E> bl;
   bl.dh_next = 0.0f;
-  auto visit = [&](const SegRaw<IO, E, KS, kCM<V>>& in, bool more, SegRaw<IO, E, KS, kCM<V>>& nxt) {
+  bl.stage = stage;
+  auto visit = [&](const SegRaw<IO, E, KS, kCM<V>, ST>& in, bool more, SegRaw<IO, E, KS, kCM<V>, ST>& nxt) {
     const int c0 = cp.seg * K;
     const int len = min(K, T - c0);
     bl.gxbase = static_cast<IO*>(ba.gx) + cp.nx0;
@@ -1512,20 +1675,25 @@ __device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const
     for (int j = 0; j < E; ++j) zero[j] = 0.0f;
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-      raw_to_float<IO, E>(in.in.x[k], xin[k]);
+      uint32_t raw[W];
+      slot_to_lane<W, ST>(in.in.x[k], stage, raw);
+      raw_to_float<IO, E>(raw, xin[k]);
       gsv[k] = raw_to_float<IO>(in.in.gs[k]);
     }
+    float gvv[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) gvv[k] = FAST ? 0.0f : in.in.gv[k];
     Stash<BL, KS, V> st;
-    recompute_chunk<BL, L, V, KS>(a, br, 0.0f, zero, in.h0, cp.seg > 0 && in.h0 >= a.vth, xin, st);
+    recompute_chunk<BL, L, V, KS, FAST>(a, br, 0.0f, zero, in.h0, cp.seg > 0 && in.h0 >= a.vth, xin, st);
     if (more) {
-      load_segment_raw<IO, BL, L, V, KS>(ba, lo, ld.n0, ld.nx0, ld.seg, nxt);
+      load_segment_raw<IO, BL, L, V, KS, !FAST, ST>(ba, lo, ld.n0, ld.nx0, ld.seg, nxt);
       next(ld);
     }
-    reverse_chunk<IO, BL, L, V, KS, true>(ba, lo, br, 0.0f, beta_r, c0, st, gsv, in.in.gv, bl, acc, len);
+    reverse_chunk<IO, BL, L, V, KS, true, ST>(ba, lo, br, 0.0f, beta_r, c0, st, gsv, gvv, bl, acc, len);
     next(cp);
   };
   for (int i = 0; i + 1 < nvis; ++i) {
-    SegRaw<IO, E, KS, kCM<V>> nxt;
+    SegRaw<IO, E, KS, kCM<V>, ST> nxt;
     visit(cur, true, nxt);
     cur = nxt;
   }
@@ -1646,12 +1814,55 @@ __device__ __forceinline__ void reduce_partials(const BwdArgs& ba, const Pos& po
   }
 }
 
+// The backward of the lane's neurons: the short-sequence pipeline (T = KS),
+// the Stateless segment pipeline (K <= KS), or neuron by neuron.  ST: wide rows
+// staged (see load_pieces; lo.xw is the wave's stretch).
+template <typename IO, int BL, int L, int V, int KS, bool ST>
+__device__ __forceinline__ void bwd_run(const BwdArgs& ba, const LaneOff& lo, const Branches<BL, kKC<V>>& br,
+                                        float alpha, int64_t bt0, int nk, Accum<BL, BL * kKC<V>>& acc,
+                                        uint32_t* stage) {
+  const ScanArgs& a = ba.s;
+  const int T = int(a.T);
+  // Without a gated-off branch in the wave (no mask, or a channel whose
+  // branches are all on) and without grad_v_soma, the pipelines run a copy
+  // without the per-step gate select and without grad_v_soma requests (bf16
+  // ImageNet-stem layer: 434 -> 396 VALU instructions per neuron; bf16 backward
+  // 1-2 % faster without the empty loads).  The vote is wave-uniform, so each
+  // wave runs one copy.
+  bool all_on = true;
+#pragma unroll
+  for (int j = 0; j < BL; ++j) all_on = all_on && br.on[j];
+  const bool fast = __all(all_on) && !ba.gv;
+  if constexpr (KS == 4) {
+    if (T == KS) {
+      if (fast) single_chunk_items<IO, BL, L, V, KS, true, ST>(ba, lo, br, alpha, bt0, nk, acc, stage);
+      else single_chunk_items<IO, BL, L, V, KS, false, ST>(ba, lo, br, alpha, bt0, nk, acc, stage);
+      return;
+    }
+  }
+  if constexpr (kSL<V>) {
+    if (a.K <= KS) {
+      if (fast) stateless_segment_items<IO, BL, L, V, KS, true, ST>(ba, lo, br, bt0, nk, acc, stage);
+      else stateless_segment_items<IO, BL, L, V, KS, false, ST>(ba, lo, br, bt0, nk, acc, stage);
+      return;
+    }
+  }
+  for (int i = 0; i < nk; ++i)
+    backward_neuron<IO, BL, L, V, KS, false>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc, stage);
+}
+
 template <typename IO, int BL, int L, int V, int KS>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BL * kKC<V> * KS <= 8 ? 4 : (BL * kKC<V> * KS <= 16 ? 3 : 2)))) dendsn_bwd_kernel(BwdArgs ba) {
   constexpr int E = BL * kKC<V>;
+  constexpr int W = kRawW<IO, E, kCM<V>>;
+  // Staged wide rows (see load_pieces) for the Stateless Dendrite's pipelines:
+  // the stateful dendrite's stash of a wide lane left no room for the pieces
+  // (its staged short-sequence copy spilled in the loop).
+  constexpr bool kWide = kWideRow<IO, E, kCM<V>> && kSL<V>;
   if (ba.s.beta_p) ba.s.beta = ba.s.beta_p[0];  // learnable (PLIF) decay
   const ScanArgs& a = ba.s;
   const Pos pos = locate<L>(a);
+  const bool full = kWide && __all(pos.active);
   Accum<BL, E> acc;
 #pragma unroll
   for (int j = 0; j < BL; ++j) acc.k[j] = acc.z[j] = 0.0f;
@@ -1663,37 +1874,22 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     Branches<BL, kKC<V>> br;
     load_branches<BL, kKC<V>>(a, pos.c, pos.sub, br);
     const float alpha = a.alpha ? a.alpha[0] : 0.0f;
-    const LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
+    LaneOff lo = lane_offsets<IO, E, kCM<V>>(a, pos);
     int64_t bt0;
     const int nk = items_of(a, pos, &bt0);
-    const int T = int(a.T);
-    bool single = false;
-    if constexpr (KS == 4) {
-      if (T == KS) {
-        // Without a gated-off branch in the wave (no mask, or a channel whose
-        // branches are all on) and without grad_v_soma, the recompute runs
-        // without the per-step gate select and no grad_v_soma rows are
-        // requested (bf16 ImageNet-stem layer: 434 -> 396 VALU instructions per
-        // neuron; bf16 backward 1-2 % faster without the empty loads).  The
-        // vote is wave-uniform, so each wave runs one copy.
-        bool all_on = true;
-#pragma unroll
-        for (int j = 0; j < BL; ++j) all_on = all_on && br.on[j];
-        if (__all(all_on) && !ba.gv) single_chunk_items<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc);
-        else single_chunk_items<IO, BL, L, V, KS>(ba, lo, br, alpha, bt0, nk, acc);
-        single = true;
+    bool done = false;
+    if constexpr (kWide) {
+      __shared__ uint32_t stage[kThreads / 64][64 * W];
+      lo.xw = __builtin_amdgcn_readfirstlane(lo.x);
+      // staged where the loads are too: the two pipelines (the neuron-by-neuron
+      // path keeps lane loads and stores)
+      const bool pipelined = (KS == 4 && int(a.T) == KS) || a.K <= KS;
+      if (full && pipelined && stage_rows<IO>(a, lo.xw, bt0)) {
+        bwd_run<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc, stage[threadIdx.x >> 6]);
+        done = true;
       }
     }
-    if constexpr (kSL<V>) {
-      if (!single && a.K <= KS) {
-        stateless_segment_items<IO, BL, L, V, KS>(ba, lo, br, bt0, nk, acc);
-        single = true;
-      }
-    }
-    if (!single) {
-      for (int i = 0; i < nk; ++i)
-        backward_neuron<IO, BL, L, V, KS>(ba, lo, bt0 + int64_t(i) * a.ways, br, alpha, acc);
-    }
+    if (!done) bwd_run<IO, BL, L, V, KS, false>(ba, lo, br, alpha, bt0, nk, acc, nullptr);
   }
   if (pos.sub != 0) acc.b = 0.0f;  // the soma runs in every lane of a neuron: count it once
   // every thread of the block reaches this one call (it holds block barriers)

@@ -61,6 +61,7 @@ struct ScanArgs {
   int32_t mode, ways, pb, tpc, cpt, bpg;
   int32_t nw;           // spatial tiles: a lane takes positions p, p + 64 / L, ... (nw of them)
   int32_t xk;           // runs of xk consecutive blocks share an XCD (see locate)
+  int32_t stg;          // 1: a sample's slice of X is a multiple of 16 bytes (wide rows may be staged)
   int64_t ntiles;
 };
 
