@@ -79,29 +79,37 @@ __device__ __forceinline__ bf16_t to_bf16(float a) {
 }
 
 // Streaming loads are non-temporal: X, grad_spikes and checkpoints are read
-// once per pass, so they should not displace anything in the caches.
+// once per pass, so they should not displace anything in the caches.  A lane
+// row of more than 16 bytes takes several loads that each touch every cache
+// line of the wave's stretch; those use the default policy, so that the later
+// loads of a row find the lines the first brought in (non-temporal, a copy of
+// 40-byte lane pieces ran at 1.9 TB/s against 4.6-4.9 with the default policy).
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
+template <typename T>
+__device__ __forceinline__ T stream_load(const T* p, bool cached);
+
 template <int BL>
 __device__ __forceinline__ void load_vec(const float* __restrict__ p, float (&v)[BL]) {
+  constexpr bool wide = BL * 4 > 16;
   if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
-      const f32x4_t q = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p) + i);
+      const f32x4_t q = stream_load(reinterpret_cast<const f32x4_t*>(p) + i, wide);
       v[4 * i] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
     }
   } else if constexpr (BL % 2 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 2; ++i) {
-      const f32x2_t q = __builtin_nontemporal_load(reinterpret_cast<const f32x2_t*>(p) + i);
+      const f32x2_t q = stream_load(reinterpret_cast<const f32x2_t*>(p) + i, wide);
       v[2 * i] = q.x; v[2 * i + 1] = q.y;
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < BL; ++i) v[i] = __builtin_nontemporal_load(p + i);
+    for (int i = 0; i < BL; ++i) v[i] = stream_load(p + i, wide);
   }
 }
 
@@ -158,6 +166,7 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
 
 template <int BL>
 __device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL], const float*) {
+  constexpr int kAuxNT = BL * 4 > 16 ? 0 : dendsn::kAuxNT;  // (see load_vec)
   if constexpr (BL % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 4; ++i) {
@@ -179,6 +188,7 @@ __device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL]
 
 template <int BL>
 __device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL], const bf16_t*) {
+  constexpr int kAuxNT = BL * 2 > 16 ? 0 : dendsn::kAuxNT;  // (see load_vec)
   if constexpr (BL % 8 == 0) {
 #pragma unroll
     for (int i = 0; i < BL / 8; ++i) {
