@@ -168,6 +168,10 @@ KC_SHAPES = [
     (4, 2, 6, 130, 2, 2, "bf16", 4),     # generic bf16
     (6, 3, 4, 3, 1, 4, "bf16", 6),       # generic bf16, k = 4
     (3, 2, 5, 17, 1, 2, "f32", 3),       # generic, one branch
+    # wide lane rows staged through LDS (full, aligned waves) beside unstaged ones
+    (4, 2, 3, 300, 5, 2, "f32", 4),      # generic P = 10, conv tiles: a ragged last tile
+    (4, 2, 4, 96, 5, 2, "bf16", 4),      # generic bf16 P = 10 (20-byte lane rows), one chunk
+    (10, 2, 4, 96, 5, 2, "bf16", 4),     # the same over three checkpoint segments
 ]
 
 
