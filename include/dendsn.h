@@ -185,11 +185,11 @@ dendsn_status dendsn_backward(const dendsn_cfg* cfg, const void* x, const float*
                               size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Maximum workspace of dendsn_backward_noalloc: 16 MiB of device memory per
+ * Maximum workspace of dendsn_backward_noalloc: 32 MiB of device memory per
  * GPU, held by the library from the first call on that GPU until the process
- * ends (every benchmark-sized layer needs at most 12.1 MiB).
+ * ends (every benchmark-sized layer needs at most 25.2 MiB).
  */
-#define DENDSN_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+#define DENDSN_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
 
 /*
  * dendsn_backward for callers that cannot allocate device memory (code under

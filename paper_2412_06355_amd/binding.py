@@ -22,7 +22,7 @@ PSI = {"identity": 0, "mexhat": 1}
 SG = {"atan": 0, "sigmoid": 1}
 LAYOUT = {"npb": 0, "channel_major": 1}
 
-NOALLOC_SCRATCH_BYTES = 16 << 20   # DENDSN_NOALLOC_SCRATCH_BYTES of include/dendsn.h
+NOALLOC_SCRATCH_BYTES = 32 << 20   # DENDSN_NOALLOC_SCRATCH_BYTES of include/dendsn.h
 
 STATUS = {0: "DENDSN_OK", 1: "DENDSN_E_INVALID", 2: "DENDSN_E_UNSUPPORTED",
           3: "DENDSN_E_WORKSPACE", 4: "DENDSN_E_HIP"}

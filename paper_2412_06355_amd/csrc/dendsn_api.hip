@@ -278,7 +278,13 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
     p.tpc = int32_t(ceil_div(c->S, p.pb)); p.cpt = 1;
     p.ntiles = c->C * p.tpc;
   } else if (c->S == 1) {
-    p.mode = kFC; p.ways = 4; p.pb = 64 / L;
+    // Four batch ways of 64 / L channels, or in the backward of neurons over 8
+    // or more lanes two ways of 128 / L channels: then each way's two waves read
+    // adjacent halves of the same grad_spikes lines at about the same time (with
+    // 8 channels a wave reads a quarter line per row).  Measured on MI355X: the
+    // gated 32-branch layer's backward -3.6 % (twice the partial slots
+    // included), the long-horizon layer (4 lanes) unchanged either way.
+    p.mode = kFC; p.ways = (bwd && L >= 8) ? 2 : 4; p.pb = kThreads / (p.ways * L);
     p.tpc = 1; p.cpt = p.pb;
     p.ntiles = ceil_div(c->C, p.cpt);
   } else {

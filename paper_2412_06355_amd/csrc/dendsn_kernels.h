@@ -765,7 +765,7 @@ __device__ __forceinline__ Pos locate(const ScanArgs& a) {
   // accesses per row is contiguous across the wave.
   constexpr int kSlots = 64 / L;
   r.p = a.nw > 1 ? (q / kSlots) * (a.nw * kSlots) + q % kSlots : q % a.pb;
-  // Batch ways are whole waves (kFC: pb * L == 64) or a single way, so the way
+  // Batch ways are whole waves (kFC: pb * L is 64 or 128) or a single way, so the way
   // index is wave-uniform; readfirstlane lets the compiler keep it scalar.
   r.way = __builtin_amdgcn_readfirstlane(q / a.pb);
   // Blocks are dealt to the 8 XCDs round-robin; with xk > 1 block b takes the
