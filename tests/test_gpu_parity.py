@@ -66,6 +66,10 @@ SHAPES = [
     (6, 2, 20, 1, 16, "bf16", 3),     # bf16 backward splits a neuron differently from the forward
     (4, 2, 9, 40, 32, "bf16", 4),
     (5, 2, 3, 1, 64, "bf16", 2),
+    # fully connected, 8 or more lanes per neuron: the backward's two batch ways
+    # with an odd batch and a last tile of one channel
+    (5, 3, 33, 1, 32, "f32", 2),
+    (4, 3, 17, 1, 32, "bf16", 4),
 ]
 
 
