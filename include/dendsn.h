@@ -57,9 +57,12 @@
  *     first failed check is available from dendsn_last_error() on the calling
  *     thread.  A failed launch returns DENDSN_E_HIP.  Faults inside a kernel
  *     surface at the caller's next synchronisation.
- *   - An empty layer (T, batch, C or S of 0) is refused with DENDSN_E_INVALID:
- *     there is nothing to compute and no gradient to define, so the caller skips
- *     the call.
+ *   - An empty layer (T, batch, C or S of 0) is valid: dendsn_forward has no
+ *     output element to write and launches nothing; dendsn_backward (and
+ *     dendsn_backward_noalloc) write +0 to every parameter gradient requested,
+ *     the value of a sum with no terms.  Pointers to arrays of no elements may
+ *     be NULL there (x, spikes, grad_spikes, grad_x; kappa when C = 0);
+ *     dendsn_ckpt_bytes is 0 and dendsn_bwd_workspace_bytes stays positive.
  *   - Size limits, refused with DENDSN_E_UNSUPPORTED: one sample's slice of X
  *     (C * S * P elements) must stay below 4 GiB, since lanes address it with
  *     32-bit byte offsets (whole tensors may be larger); the grid must stay below
@@ -95,10 +98,10 @@ typedef enum dendsn_sg { DENDSN_SG_ATAN = 0, DENDSN_SG_SIGMOID = 1 } dendsn_sg;
 typedef enum dendsn_layout { DENDSN_LAYOUT_NPB = 0, DENDSN_LAYOUT_CHANNEL_MAJOR = 1 } dendsn_layout;
 
 typedef struct dendsn_cfg {
-    int64_t T;                 /* time steps, >= 1                                         */
-    int64_t batch;             /* batch items, >= 1                                        */
-    int64_t C;                 /* channels (parameter sets), >= 1                          */
-    int64_t S;                 /* spatial positions per channel, >= 1 (1 = fully connected)*/
+    int64_t T;                 /* time steps, >= 0 (0: an empty layer)                     */
+    int64_t batch;             /* batch items, >= 0                                        */
+    int64_t C;                 /* channels (parameter sets), >= 0                          */
+    int64_t S;                 /* spatial positions per channel, >= 0 (1 = fully connected)*/
     int32_t B;                 /* branches per neuron, 1..128                              */
     int32_t comps_per_branch;  /* compartments per branch KC = P / B: 1, 2 or 4            */
     int32_t stateful;          /* 1: leaky compartments; 0: Stateless Dendrite             */
@@ -123,8 +126,8 @@ typedef struct dendsn_cfg {
  * steps K, 2K, ... < T: nck * N * (P + 1) * 4 bytes for a stateful dendrite (the
  * P compartment states and the somatic potential), nck * N * 4 for the
  * Stateless Dendrite (only the somatic potential: its compartment state is the
- * input itself).  Zero when K >= T.  Returns DENDSN_E_INVALID / _UNSUPPORTED
- * for a bad cfg.
+ * input itself).  Zero when K >= T or the layer is empty.  Returns
+ * DENDSN_E_INVALID / _UNSUPPORTED for a bad cfg.
  */
 dendsn_status dendsn_ckpt_bytes(const dendsn_cfg* cfg, size_t* bytes);
 

@@ -137,6 +137,16 @@ def _check_shapes(X, kappa, C, S, k):
     if X.ndim != 3:
         raise ValueError("X must be [T, N, P]")
     T, N, P = X.shape
+    if C * S == 0:
+        # A layer without neurons: every per-neuron array is empty and every
+        # sum over neurons has no terms, whatever the batch size.
+        if N != 0:
+            raise ValueError("N must be batch * C * S")
+        if k < 1 or P % k != 0:
+            raise ValueError("P must be a multiple of the compartments per branch k")
+        if kappa.shape != (C, P // k):
+            raise ValueError("kappa must be [C, B]")
+        return T, N, P, P // k, 0
     if N % (C * S) != 0:
         raise ValueError("N must be batch * C * S")
     if k < 1 or P % k != 0:

@@ -188,12 +188,21 @@ bool cm_mapping(int B, int KC, int* BL, int* L) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// No neuron-step at all (T = 0 or N = 0): the forward has nothing to compute
+// and the backward's parameter gradients are empty sums, +0.
+bool empty_layer(const dendsn_cfg* c) { return c->T == 0 || c->batch == 0 || c->C == 0 || c->S == 0; }
+
+// Workspace of an empty layer: nothing is read or written there, but the size
+// stays positive like every other layer's.
+constexpr size_t kEmptyWorkspace = 256;
+
 dendsn_status check_cfg(const dendsn_cfg* c) {
   if (!c) return fail(DENDSN_E_INVALID, "cfg is NULL");
-  if (c->T < 1 || c->T > INT32_MAX) return fail(DENDSN_E_INVALID, "T must be in [1, 2^31)");
-  if (c->batch < 1) return fail(DENDSN_E_INVALID, "batch must be >= 1");
-  if (c->C < 1) return fail(DENDSN_E_INVALID, "C must be >= 1");
-  if (c->S < 1) return fail(DENDSN_E_INVALID, "S must be >= 1");
+  // Zero steps, samples, channels or positions make an empty layer (valid).
+  if (c->T < 0 || c->T > INT32_MAX) return fail(DENDSN_E_INVALID, "T must be in [0, 2^31)");
+  if (c->batch < 0) return fail(DENDSN_E_INVALID, "batch must be >= 0");
+  if (c->C < 0) return fail(DENDSN_E_INVALID, "C must be >= 0");
+  if (c->S < 0) return fail(DENDSN_E_INVALID, "S must be >= 0");
   if (c->B < 1 || c->B > 128) return fail(DENDSN_E_INVALID, "B must be in [1, 128]");
   if (c->comps_per_branch < 1) return fail(DENDSN_E_INVALID, "comps_per_branch must be >= 1");
   if (c->comps_per_branch != 1 && c->comps_per_branch != 2 && c->comps_per_branch != 4)
@@ -215,10 +224,12 @@ dendsn_status check_cfg(const dendsn_cfg* c) {
     return fail(DENDSN_E_INVALID, "bad layout");
   // N and T * N * B must fit comfortably in int64 element counts.
   const int64_t lim = int64_t(1) << 46;
-  if (c->batch > lim / c->C || c->batch * c->C > lim / c->S) return fail(DENDSN_E_INVALID, "N too large");
+  if (c->C > lim || c->S > lim) return fail(DENDSN_E_INVALID, "C or S too large");
+  if (c->C > 0 && c->S > 0 && (c->batch > lim / c->C || c->batch * c->C > lim / c->S))
+    return fail(DENDSN_E_INVALID, "N too large");
   const int64_t N = c->batch * c->C * c->S;
   const int64_t P = int64_t(c->B) * c->comps_per_branch;
-  if (N > (lim / P) / c->T) return fail(DENDSN_E_INVALID, "T * N * P too large");
+  if (c->T > 0 && N > (lim / P) / c->T) return fail(DENDSN_E_INVALID, "T * N * P too large");
   int BL, L, fast;
   if (channel_major(c)) {
     if (!cm_mapping(c->B, c->comps_per_branch, &BL, &L))
@@ -407,7 +418,7 @@ dendsn_status dendsn_ckpt_bytes(const dendsn_cfg* cfg, size_t* bytes) {
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
   if (!bytes) return fail(DENDSN_E_INVALID, "bytes is NULL");
-  *bytes = ckpt_bytes(cfg, make_plan(cfg, false));
+  *bytes = empty_layer(cfg) ? 0 : ckpt_bytes(cfg, make_plan(cfg, false));
   return DENDSN_OK;
 }
 
@@ -416,6 +427,10 @@ dendsn_status dendsn_bwd_workspace_bytes(const dendsn_cfg* cfg, size_t* bytes) {
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
   if (!bytes) return fail(DENDSN_E_INVALID, "bytes is NULL");
+  if (empty_layer(cfg)) {
+    *bytes = kEmptyWorkspace;
+    return DENDSN_OK;
+  }
   size_t offA, total;
   ws_layout(cfg, make_plan(cfg, true), &offA, &total);
   *bytes = total;
@@ -428,9 +443,10 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   g_last_error.clear();
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
-  if (!x) return fail(DENDSN_E_INVALID, "x is NULL");
-  if (!kappa) return fail(DENDSN_E_INVALID, "kappa is NULL");
-  if (!spikes) return fail(DENDSN_E_INVALID, "spikes is NULL");
+  const bool empty = empty_layer(cfg);  // arrays of no elements may be NULL
+  if (!x && !empty) return fail(DENDSN_E_INVALID, "x is NULL");
+  if (!kappa && cfg->C > 0) return fail(DENDSN_E_INVALID, "kappa is NULL");
+  if (!spikes && !empty) return fail(DENDSN_E_INVALID, "spikes is NULL");
   if (cfg->stateful && !alpha) return fail(DENDSN_E_INVALID, "alpha is NULL for a stateful dendrite");
   const size_t esz = cfg->io == DENDSN_IO_BF16 ? 2 : 4;
   if (!aligned(x, 16)) return fail(DENDSN_E_INVALID, "x must be 16-byte aligned");
@@ -439,6 +455,7 @@ dendsn_status dendsn_forward(const dendsn_cfg* cfg, const void* x, const float* 
   if ((alpha && !aligned(alpha, 4)) || (beta && !aligned(beta, 4)) || !aligned(kappa, 4) ||
       (xi && !aligned(xi, 4)) || (zeta && !aligned(zeta, 4)) || (v_soma && !aligned(v_soma, 4)))
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
+  if (empty) return DENDSN_OK;  // every output has no elements
   const Plan p = make_plan(cfg, false);
   if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
   FwdArgs fa;
@@ -502,6 +519,27 @@ dendsn_status scratch_on_stream_device(hipStream_t stream, void** out) {
   return DENDSN_OK;
 }
 
+// The backward of an empty layer: the finalize kernel over no partial slots
+// writes +0 to every requested parameter gradient (a fill kernel, so the call
+// records no memset node when captured into a graph).
+dendsn_status zero_param_grads(const dendsn_cfg* cfg, const uint8_t* mask, float* grad_alpha, float* grad_beta,
+                               float* grad_kappa, float* grad_xi, float* grad_zeta, hipStream_t stream) {
+  FinArgs f;
+  memset(&f, 0, sizeof(f));
+  f.mask = mask;
+  f.gk = grad_kappa; f.gxi = grad_xi; f.gz = grad_zeta; f.ga = grad_alpha; f.gb = grad_beta;
+  f.C = cfg->C; f.B = cfg->B; f.P = cfg->B * cfg->comps_per_branch; f.KC = cfg->comps_per_branch;
+  f.slots = 0; f.wide = 0; f.nA = 0;
+  f.stateful = cfg->stateful;
+  const int64_t nout = cfg->C * (2 * cfg->B + f.P);
+  if (ceil_div(nout, kThreads) + 2 > int64_t(INT32_MAX))
+    return fail(DENDSN_E_UNSUPPORTED, "too many parameter-gradient outputs");
+  dendsn_finalize_kernel<<<dim3(unsigned(ceil_div(nout, kThreads) + 2)), dim3(kThreads), 0, stream>>>(f);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(DENDSN_E_HIP, std::string("finalize launch: ") + hipGetErrorString(e));
+  return DENDSN_OK;
+}
+
 // The backward on the caller's workspace or, with own_scratch, on the
 // library's scratch array of the stream's device (every argument is checked
 // before the array's address is looked up).
@@ -513,12 +551,15 @@ dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* a
                             hipStream_t stream) {
   dendsn_status st = check_cfg(cfg);
   if (st != DENDSN_OK) return st;
-  if (!x) return fail(DENDSN_E_INVALID, "x is NULL");
-  if (!kappa) return fail(DENDSN_E_INVALID, "kappa is NULL");
-  if (!grad_spikes) return fail(DENDSN_E_INVALID, "grad_spikes is NULL");
-  if (!grad_x) return fail(DENDSN_E_INVALID, "grad_x is NULL");
+  const bool empty = empty_layer(cfg);  // arrays of no elements may be NULL
+  if (!x && !empty) return fail(DENDSN_E_INVALID, "x is NULL");
+  if (!kappa && cfg->C > 0) return fail(DENDSN_E_INVALID, "kappa is NULL");
+  if (!grad_spikes && !empty) return fail(DENDSN_E_INVALID, "grad_spikes is NULL");
+  if (!grad_x && !empty) return fail(DENDSN_E_INVALID, "grad_x is NULL");
   if (cfg->stateful && !alpha) return fail(DENDSN_E_INVALID, "alpha is NULL for a stateful dendrite");
-  const Plan p = make_plan(cfg, true);
+  Plan p;
+  memset(&p, 0, sizeof(p));
+  if (!empty) p = make_plan(cfg, true);
   if (p.nck > 0 && !ckpt) return fail(DENDSN_E_INVALID, "ckpt is NULL but the forward wrote checkpoints");
   const size_t esz = cfg->io == DENDSN_IO_BF16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(grad_x, 16)) return fail(DENDSN_E_INVALID, "x / grad_x must be 16-byte aligned");
@@ -530,8 +571,8 @@ dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* a
       (grad_kappa && !aligned(grad_kappa, 4)) ||
       (grad_xi && !aligned(grad_xi, 4)) || (grad_zeta && !aligned(grad_zeta, 4)))
     return fail(DENDSN_E_INVALID, "fp32 tensor misaligned");
-  size_t offA, total;
-  ws_layout(cfg, p, &offA, &total);
+  size_t offA = 0, total = kEmptyWorkspace;
+  if (!empty) ws_layout(cfg, p, &offA, &total);
   if (own_scratch) {
     if (total > kScratchBytes)
       return fail(DENDSN_E_WORKSPACE, "layer needs " + std::to_string(total) +
@@ -543,6 +584,7 @@ dendsn_status backward_impl(const dendsn_cfg* cfg, const void* x, const float* a
     if (workspace_bytes < total)
       return fail(DENDSN_E_WORKSPACE, "workspace smaller than dendsn_bwd_workspace_bytes()");
   }
+  if (empty) return zero_param_grads(cfg, mask, grad_alpha, grad_beta, grad_kappa, grad_xi, grad_zeta, stream);
   if ((st = check_grid(cfg, p)) != DENDSN_OK) return st;
   if (own_scratch && (st = scratch_on_stream_device(stream, &workspace)) != DENDSN_OK) return st;
 

@@ -98,7 +98,8 @@ def test_workspace_bytes_positive_and_grows_with_groups(lib):
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(T=0), E_INVALID), (dict(batch=0), E_INVALID), (dict(C=0), E_INVALID), (dict(S=0), E_INVALID),
+    (dict(T=-1), E_INVALID), (dict(batch=-1), E_INVALID), (dict(C=-1), E_INVALID), (dict(S=-1), E_INVALID),
+    (dict(T=1 << 31), E_INVALID), (dict(C=1 << 50, S=0), E_INVALID), (dict(B=0, T=0), E_INVALID),
     (dict(B=0), E_INVALID), (dict(B=129), E_INVALID), (dict(comps_per_branch=0), E_INVALID),
     (dict(comps_per_branch=3), E_UNSUPPORTED), (dict(comps_per_branch=8), E_UNSUPPORTED),
     (dict(B=12, comps_per_branch=2), E_UNSUPPORTED), (dict(B=5, comps_per_branch=4), E_UNSUPPORTED),
@@ -150,6 +151,30 @@ def test_forward_argument_checks(lib):
     assert bwd(lib, cfg, grad_beta=GOOD + 0x702) == E_INVALID
     assert fwd(lib, cfg, ckpt=GOOD + 8) == E_INVALID
     assert "align" in dendsn.dendsn_last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(T=0), dict(batch=0), dict(C=0), dict(S=0), dict(T=0, batch=0, C=0, S=0),
+                                dict(T=0, ckpt_every=1), dict(batch=0, T=64, ckpt_every=8, B=16),
+                                dict(S=0, C=8, B=8, layout=1), dict(C=0, io=1, B=8, comps_per_branch=2)])
+def test_empty_layers_are_valid(lib, kw):
+    """An empty layer (no neuron-step) is a valid call: no checkpoint bytes, a
+    positive workspace, and a forward that accepts NULL for its arrays of no
+    elements and launches nothing (so it returns OK without a GPU)."""
+    cfg = base_cfg(**kw)
+    out = ctypes.c_size_t(12345)
+    assert lib.dendsn_ckpt_bytes(ctypes.byref(cfg), ctypes.byref(out)) == OK
+    assert out.value == 0
+    assert lib.dendsn_bwd_workspace_bytes(ctypes.byref(cfg), ctypes.byref(out)) == OK
+    assert out.value > 0
+    kappa = None if cfg.C == 0 else GOOD + 0x200
+    assert fwd(lib, cfg, x=None, spikes=None, kappa=kappa) == OK
+    assert fwd(lib, cfg, x=None, spikes=None, kappa=kappa, alpha=None) == E_INVALID  # stateful needs alpha
+    assert fwd(lib, cfg, x=GOOD + 4, spikes=None, kappa=kappa) == E_INVALID            # alignment still checked
+    if cfg.C > 0:
+        assert fwd(lib, cfg, x=None, spikes=None, kappa=None) == E_INVALID
+    # the backward's host checks run as for any layer (its launch needs a GPU)
+    assert bwd(lib, cfg, x=None, gx=None, gs=None, ws=None) == E_WORKSPACE
+    assert bwd(lib, cfg, x=None, gx=None, gs=None, ws_bytes=16) == E_WORKSPACE
 
 
 def test_backward_argument_checks(lib):

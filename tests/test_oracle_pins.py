@@ -785,3 +785,31 @@ def test_compartment_order_within_a_branch_does_not_matter():
     swap[[0, k]] = swap[[k, 0]]   # compartment 0 to branch 1 and back
     c3 = dict(case, X=case["X"][:, :, swap], xi=case["xi"][:, swap])
     assert not np.allclose(run_oracle(c3)["H"], a["H"], rtol=1e-6)
+
+
+@pytest.mark.parametrize("T,batch,C,S", [(0, 2, 3, 4), (5, 0, 3, 4), (5, 2, 0, 4), (5, 2, 3, 0), (0, 0, 0, 0)])
+def test_empty_layer_has_empty_outputs_and_zero_gradients(T, batch, C, S):
+    """A layer with no neuron-step: every output has no elements and every
+    parameter gradient is a sum with no terms, +0; the same layer with one more
+    step or sample is not empty (the shapes follow the layer, not a special case)."""
+    B, k = 3, 2
+    N, P = batch * C * S, B * k
+    rng = np.random.default_rng(2)
+    kw = dict(alpha=0.5, beta=0.5, v_th=1.0, kappa=rng.random((C, B)), xi=rng.random((C, P)),
+              zeta=rng.random((C, B)) + 0.5, mask=(rng.random((C, B)) < 0.5).astype(np.uint8), C=C, S=S,
+              comps_per_branch=k, residual=True)
+    rec = oracle.forward(np.zeros((T, N, P)), **kw)
+    assert rec["S"].shape == (T, N) and rec["H"].shape == (T, N)
+    g = oracle.backward(rec, np.zeros((T, N)))
+    assert g["gX"].shape == (T, N, P)
+    for name, shape in (("g_kappa", (C, B)), ("g_xi", (C, P)), ("g_zeta", (C, B))):
+        assert g[name].shape == shape
+        assert not g[name].any() and not np.signbit(g[name]).any()
+    assert g["g_alpha"] == 0.0 and g["g_beta"] == 0.0
+    assert not math.copysign(1.0, g["g_alpha"]) < 0 and not math.copysign(1.0, g["g_beta"]) < 0
+    if C * S > 0 and batch > 0:
+        rec1 = oracle.forward(np.ones((T + 1, N, P)), **kw)
+        g1 = oracle.backward(rec1, np.ones((T + 1, N)))
+        assert np.abs(g1["g_kappa"]).sum() > 0
+    with pytest.raises(ValueError):
+        oracle.forward(np.zeros((T, 1, P)), **dict(kw, C=0)) if C == 0 else oracle.forward(np.zeros((T, N + 1, P)), **kw)
