@@ -331,7 +331,11 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   // slower with one lane per neuron; with 8-byte rows (bf16, four branches) or
   // the fully connected tiling the cap costs 15-17 %.  Unused dynamic LDS
   // reserves the room.
-  const bool cap = bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16 && (p.nw == 1 || p.L >= 2);
+  // The stateful dendrite's wide fp32 lanes (more than 16 bytes of a row in a
+  // lane) already hold about 70 KB of static LDS per block in the backward (the
+  // DMA areas of their segment pipeline), which keeps them at two blocks per CU.
+  const bool wide_sf = !p.cm && c->stateful && esz == 4 && p.BL * p.KC * esz > 16;
+  const bool cap = bwd && p.mode == kSpatial && p.BL * p.KC * esz >= 16 && (p.nw == 1 || p.L >= 2) && !wide_sf;
   p.lds = cap ? int32_t(163840 / 3 + 256) : 0;
   // XCD runs (blocks are dealt to the 8 XCDs round-robin; measured on MI355X):
   // fully connected tiles in runs of 32 blocks per XCD (dbg forward / backward

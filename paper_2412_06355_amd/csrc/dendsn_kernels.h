@@ -164,6 +164,12 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
 }
 
+// A wave-uniform value the compiler cannot prove uniform (a select on loop
+// state inside the lanes' active region) made explicit: as part of a buffer
+// resource it would otherwise be fed to the load through a per-lane loop over
+// distinct values, whose first wait drains every request in flight.
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
 template <int BL>
 __device__ __forceinline__ void bload_vec(rsrc_t r, uint32_t off, float (&v)[BL], const float*) {
   constexpr int kAuxNT = BL * 4 > 16 ? 0 : dendsn::kAuxNT;  // (see load_vec)
@@ -541,6 +547,40 @@ __device__ __forceinline__ void slot_to_lane(const uint32_t (&slot)[kSlotW<W, ST
   } else {
 #pragma unroll
     for (int j = 0; j < W; ++j) out[j] = slot[j];
+  }
+}
+
+// The same pieces moved by the memory unit straight into LDS (buffer loads
+// with the LDS-DMA form): round i writes the 64 lanes' 16-byte pieces to dwords
+// 256 i + 4 lane .. + 3 of `lds`, so the stretch's dword k lands at lds[k] and
+// no register holds it in flight.  A lane past the stretch in the last round
+// fetches the stretch's first piece into the slack past 64 W dwords (an area
+// holds kDmaDw dwords).  The wave reads the area only after its vector memory
+// counter has drained, and refills it only after its reads of it have
+// completed (LDS reads and the DMA's LDS writes are not ordered otherwise).
+template <int W> constexpr int kDmaDw = 256 * kPieces<W>;
+typedef __attribute__((address_space(3))) void lds_void_t;
+// s_waitcnt lgkmcnt(0), other counters untouched: every LDS access of the wave
+// has completed.
+constexpr int kWaitLds = 0xC07F;
+
+// One round: the wave's 64 pieces at byte offsets `off` (per lane) into the 256
+// dwords at `lds` (a plain function: the LDS-DMA builtin inside a template
+// instantiated by the host compilation pass is rejected there).  Default cache
+// policy: measured on MI355X, non-temporal DMA loads made the stateful P = 10
+// backward 3.5 % faster alone but the kernel launched after it (the forward)
+// 14 % slower, the whole step 0.6 % slower.
+__device__ __forceinline__ void dma_round(rsrc_t r, uint32_t off, uint32_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, 0);
+}
+
+template <int W>
+__device__ __forceinline__ void dma_pieces(rsrc_t r, uint32_t span, uint32_t* lds) {
+  const uint32_t lane = __lane_id();
+#pragma unroll
+  for (int i = 0; i < kPieces<W>; ++i) {
+    const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
+    dma_round(r, span + (in_stretch<W>(i, lane) ? d * 4 : 0u), lds + i * 256);
   }
 }
 
@@ -1628,13 +1668,14 @@ __device__ __forceinline__ void load_segment_raw(const BwdArgs& ba, const LaneOf
     r.in.gs[k] = sizeof(IO) == 4 ? __builtin_amdgcn_raw_buffer_load_b32(rg, os, 0, kAuxNT)
                                  : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(rg, os, 0, kAuxNT));
     r.in.gv[k] = GV ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                          make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, real ? ba.gvn : 0u), lo.v, 0, kAuxNT))
+                          make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, uniform_u32(real ? ba.gvn : 0u)), lo.v, 0,
+                          kAuxNT))
                     : 0.0f;  // GV = false: known absent, nothing is requested
   }
   // checkpointed H after step c0 - 1 (a buffer of no bytes for the first segment)
   const float* hp = seg > 0 ? ba.ckh + int64_t(seg - 1) * a.N + n0 : ba.gvz;
-  r.h0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(hp, seg > 0 ? 0xFFFFFFFFu : 0u), lo.v, 0,
-                                                                kAuxNT));
+  r.h0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(hp, uniform_u32(seg > 0 ? 0xFFFFFFFFu : 0u)),
+                                                                lo.v, 0, kAuxNT));
 }
 
 template <typename IO, int BL, int L, int V, int KS, bool FAST = false, bool ST = false>
@@ -1708,6 +1749,150 @@ __device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const
     cur = nxt;
   }
   visit(cur, false, cur);
+}
+
+// The stateful dendrite's wide fp32 lanes (a lane row of more than 16 bytes,
+// e.g. ten compartments), every segment one chunk (K <= KS): pipelined over the
+// lane's (neuron, segment) visits in the Stateless pipeline's order, but the
+// next visit's X rows and checkpointed compartment state travel by LDS DMA
+// (dma_pieces) into the wave's LDS area, where they wait without registers:
+// the stash of a wide stateful neuron leaves none for rows in flight.  The
+// small per-neuron rows (grad_spikes, grad_v_soma, the checkpointed H) ride in
+// registers.  The dendritic adjoint lam and dH cross segment boundaries in
+// reverse time within one neuron and restart at its last segment.  Rows past a
+// short segment's end are not fetched: the recompute runs over whatever the
+// area holds there, and the adjoint pass skips those steps.
+// The registers of a stateful wide visit in flight (its X rows and
+// checkpointed state travel to LDS): grad_spikes, grad_v_soma and H before the
+// segment.
+template <int KS>
+struct SegSmall {
+  uint32_t gs[KS];
+  float gv[KS];
+  float h0;  // somatic potential before the segment (0 for the first)
+};
+
+// Requests visit (n0, nx0, seg): X rows and the checkpointed compartment state
+// into `area` (rows past the segment's end are not fetched), the rest into r.
+template <typename IO, int BL, int V, int KS, bool FAST>
+__device__ __forceinline__ void issue_wide_segment(const BwdArgs& ba, const LaneOff& lo, int64_t n0, int64_t nx0,
+                                                   int seg, uint32_t* area, SegSmall<KS>& r) {
+  constexpr int W = BL * kKC<V>;
+  constexpr int RD = kDmaDw<W>;
+  const ScanArgs& a = ba.s;
+  const int64_t rowX = a.N * a.P;
+  const int T = int(a.T), K = a.K;
+  const int c0 = seg * K;
+  const int len = min(K, T - c0);
+  const IO* x = static_cast<const IO*>(a.x) + nx0;
+  const IO* g = static_cast<const IO*>(ba.gspk) + n0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const bool real = k < len;
+    const int t = real ? c0 + k : c0;
+    if (real) dma_pieces<W>(make_rsrc(x + int64_t(t) * rowX), lo.xw, area + k * RD);
+    r.gs[k] = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(g + int64_t(t) * a.N), real ? lo.s : 0u, 0, kAuxNT);
+    r.gv[k] = FAST ? 0.0f
+                   : __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                         make_rsrc(ba.gvz + n0 + int64_t(t) * a.N, uniform_u32(real ? ba.gvn : 0u)), lo.v, 0,
+                         kAuxNT));
+  }
+  if (seg > 0) dma_pieces<W>(make_rsrc(ba.ckpt + (int64_t(seg - 1) * a.N + n0) * a.P), lo.xw, area + KS * RD);
+  const float* hp = seg > 0 ? ba.ckh + int64_t(seg - 1) * a.N + n0 : ba.gvz;
+  r.h0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(hp, uniform_u32(seg > 0 ? 0xFFFFFFFFu : 0u)),
+                                                                lo.v, 0, kAuxNT));
+}
+
+// The stateful dendrite's wide fp32 lanes (a lane row of more than 16 bytes,
+// e.g. ten compartments), every segment one chunk (K <= KS): pipelined over the
+// lane's (neuron, segment) visits in the Stateless pipeline's order, but the
+// next visit's X rows and checkpointed compartment state travel by LDS DMA
+// (dma_pieces) into the wave's LDS area, where they wait without registers:
+// the stash of a wide stateful neuron leaves none for rows in flight.  The
+// small per-neuron rows (grad_spikes, grad_v_soma, the checkpointed H) ride in
+// registers.  The dendritic adjoint lam and dH cross segment boundaries in
+// reverse time within one neuron and restart at its last segment.  Rows past a
+// short segment's end are not fetched: the recompute runs over whatever the
+// area holds there, and the adjoint pass skips those steps.
+template <typename IO, int BL, int L, int V, int KS, bool FAST>
+__device__ __forceinline__ void stateful_segment_items(const BwdArgs& ba, const LaneOff& lo,
+                                                       const Branches<BL, kKC<V>>& br, float alpha, int64_t bt0,
+                                                       int nk, Accum<BL, BL * kKC<V>>& acc, uint32_t* area) {
+  constexpr int E = BL * kKC<V>;
+  constexpr int W = E;               // fp32 rows: one dword per compartment
+  constexpr int RD = kDmaDw<W>;      // LDS dwords per staged row
+  static_assert(sizeof(IO) == 4 && !kSL<V> && !kCM<V>, "stateful wide fp32 lanes only");
+  const ScanArgs& a = ba.s;
+  const float beta_r = ba.detach ? 0.0f : a.beta;
+  const int T = int(a.T), K = a.K;
+  const int nseg = (T + K - 1) / K;
+  const Walk wk = make_walk<L, kCM<V>>(a, int64_t(a.ways) * a.M);
+  const int nvis = wk.nw * nk * nseg;
+  if (nvis <= 0) return;
+  struct Cursor {
+    int64_t n0, nx0;
+    int seg, w;
+  };
+  auto next = [&](Cursor& c) {
+    if (c.seg > 0) { --c.seg; return; }
+    c.seg = nseg - 1;
+    const bool last_w = ++c.w == wk.nw;
+    if (last_w) c.w = 0;
+    c.n0 += last_w ? wk.dn_item : wk.dn;
+    c.nx0 += last_w ? wk.dnx_item : wk.dnx;
+  };
+  Cursor ld{bt0 * a.M, bt0 * a.M * a.P, nseg - 1, 0};
+  Cursor cp = ld;
+  SegSmall<KS> cur;
+  issue_wide_segment<IO, BL, V, KS, FAST>(ba, lo, ld.n0, ld.nx0, ld.seg, area, cur);
+  next(ld);
+  BwdLane<IO, E> bl;
+  bl.stage = nullptr;
+  bl.dh_next = 0.0f;
+  const uint32_t lane = __lane_id();
+  for (int i = 0; i < nvis; ++i) {
+    const int c0 = cp.seg * K;
+    const int len = min(K, T - c0);
+    if (cp.seg == nseg - 1) {  // the neuron's last segment: nothing after it
+      bl.dh_next = 0.0f;
+#pragma unroll
+      for (int j = 0; j < E; ++j) bl.lam[j] = 0.0f;
+    }
+    // this visit's pieces are in the area once every vector memory access of
+    // the wave has completed
+    __builtin_amdgcn_s_waitcnt(kWaitVmem);
+    asm volatile("" ::: "memory");
+    float xin[KS][E], v0[E];
+#pragma unroll
+    for (int k = 0; k < KS; ++k)
+#pragma unroll
+      for (int j = 0; j < E; ++j) xin[k][j] = __uint_as_float(area[k * RD + lane * W + j]);
+    const bool from_ckpt = cp.seg > 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {  // (read unconditionally; the first segment starts from 0)
+      const float v = __uint_as_float(area[KS * RD + lane * W + j]);
+      v0[j] = from_ckpt ? v : 0.0f;
+    }
+    float gsv[KS], gvv[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      gsv[k] = __uint_as_float(cur.gs[k]);
+      gvv[k] = cur.gv[k];
+    }
+    const float h0 = cur.h0;
+    // the area is refilled only after these reads have completed
+    __builtin_amdgcn_s_waitcnt(kWaitLds);
+    asm volatile("" ::: "memory");
+    if (i + 1 < nvis) {
+      issue_wide_segment<IO, BL, V, KS, FAST>(ba, lo, ld.n0, ld.nx0, ld.seg, area, cur);
+      next(ld);
+    }
+    Stash<BL, KS, V> st;
+    recompute_chunk<BL, L, V, KS, FAST>(a, br, alpha, v0, h0, from_ckpt && h0 >= a.vth, xin, st);
+    bl.gxbase = static_cast<IO*>(ba.gx) + cp.nx0;
+    reverse_chunk<IO, BL, L, V, KS, true, false>(ba, lo, br, alpha, beta_r, c0, st, gsv, gvv, bl, acc, len);
+    next(cp);
+  }
 }
 
 // Per channel the backward produces W = 2 B + P parameter gradients, in the
@@ -1869,10 +2054,13 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
   // the stateful dendrite's stash of a wide lane left no room for the pieces
   // (its staged short-sequence copy spilled in the loop).
   constexpr bool kWide = kWideRow<IO, E, kCM<V>> && kSL<V>;
+  // The stateful dendrite's wide fp32 lanes move their rows by LDS DMA instead
+  // (stateful_segment_items).
+  constexpr bool kWideSF = kWideRow<IO, E, kCM<V>> && !kSL<V> && sizeof(IO) == 4;
   if (ba.s.beta_p) ba.s.beta = ba.s.beta_p[0];  // learnable (PLIF) decay
   const ScanArgs& a = ba.s;
   const Pos pos = locate<L>(a);
-  const bool full = kWide && __all(pos.active);
+  const bool full = (kWide || kWideSF) && __all(pos.active);
   Accum<BL, E> acc;
 #pragma unroll
   for (int j = 0; j < BL; ++j) acc.k[j] = acc.z[j] = 0.0f;
@@ -1896,6 +2084,23 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
       const bool pipelined = (KS == 4 && int(a.T) == KS) || a.K <= KS;
       if (full && pipelined && stage_rows<IO>(a, lo.xw, bt0)) {
         bwd_run<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc, stage[threadIdx.x >> 6]);
+        done = true;
+      }
+    }
+    if constexpr (kWideSF) {
+      // one chunk per segment, and not the short-sequence case (T = KS = 4,
+      // which has its own pipeline)
+      __shared__ uint32_t area[kThreads / 64][(KS + 1) * kDmaDw<W>];
+      const uint32_t span = __builtin_amdgcn_readfirstlane(lo.x);
+      if (full && a.K <= KS && !(KS == 4 && int(a.T) == KS) && stage_rows<IO>(a, span, bt0)) {
+        lo.xw = span;
+        bool all_on = true;  // (as in bwd_run)
+#pragma unroll
+        for (int j = 0; j < BL; ++j) all_on = all_on && br.on[j];
+        if (__all(all_on) && !ba.gv)
+          stateful_segment_items<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6]);
+        else
+          stateful_segment_items<IO, BL, L, V, KS, false>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6]);
         done = true;
       }
     }

@@ -193,6 +193,55 @@ def test_compartments_per_branch(gpu_device, shape, variant):
     compare(case, run_gpu(case, gpu_device))
 
 
+# Stateful dendrite, fp32 lane rows wider than 16 bytes, one chunk per segment
+# (K <= 4) and T != 4: the segment pipeline whose rows and checkpointed state
+# arrive in LDS by DMA (full, aligned waves) beside partially active waves that
+# keep lane loads.
+WIDE_STATEFUL = [
+    # T, batch, C, S, B, k, K
+    (10, 2, 4, 96, 5, 2, 4),     # P = 10, segments 4, 4, 2; whole channels per tile, last wave partial
+    (7, 3, 2, 300, 5, 2, 4),     # conv tiles with a ragged last tile; segments 4, 3
+    (6, 2, 3, 128, 3, 2, 2),     # 24-byte lane rows, segments of 2
+    (9, 2, 2, 256, 7, 2, 3),     # 56-byte lane rows (a partial last round of pieces), segments of 3
+    (3, 2, 4, 64, 5, 2, 3),      # T < 4: one segment of 3 steps
+    (6, 2, 2, 256, 3, 4, 4),     # k = 4, 48-byte rows (whole rounds of pieces only); segments 4, 2
+]
+
+
+@pytest.mark.parametrize("shape", WIDE_STATEFUL, ids=lambda s: "T{}b{}C{}S{}B{}k{}K{}".format(*s))
+@pytest.mark.parametrize("variant", ["mh-sig", "mh-sig-mask-gv", "id-atan-detach-plif-res"])
+def test_stateful_wide_rows_segment_pipeline(gpu_device, shape, variant):
+    T, batch, C, S, B, k, K = shape
+    c = cfg(T=T, batch=batch, C=C, S=S, B=B, comps_per_branch=k, ckpt_every=K,
+            psi="identity" if variant.startswith("id") else "mexhat", sg="sigmoid" if "sig" in variant else "atan",
+            detach_reset="detach" in variant, residual="res" in variant, beta=0.7)
+    seed = zlib.crc32(repr((shape, variant)).encode()) % 1000
+    case = make_case(c, seed=seed, x_std=1.2, alpha=0.7, mask_rho=0.5 if "mask" in variant else None,
+                     with_gv="gv" in variant, name=f"wide-sf/{shape}/{variant}",
+                     beta_dev=0.8 if "plif" in variant else None)
+    compare(case, run_gpu(case, gpu_device))
+
+
+@pytest.mark.parametrize("B,k,io", [(5, 2, "f32"), (7, 2, "f32"), (5, 2, "bf16")])
+def test_wide_rows_checkpoint_interval_is_bit_invariant(gpu_device, B, k, io):
+    """K = 2 and 4 take the stateful segment pipeline (fp32), K = 12 the
+    neuron-by-neuron path: spikes and every gradient agree bit for bit."""
+    import torch
+
+    base = cfg(T=12, batch=2, C=4, S=64, B=B, comps_per_branch=k, io=io, beta=0.8, ckpt_every=4)
+    case = make_case(base, seed=41 + B, x_mean=0.1, alpha=0.7, mask_rho=0.6, name=f"wide-ckpt/{B}/{io}")
+    d = to_device(case, gpu_device)
+    outs = []
+    for K in (4, 12, 2):
+        case.cfg = base.with_(ckpt_every=K)
+        outs.append(run_gpu(case, gpu_device, dev=d)["raw"])
+    for o in outs[1:]:
+        assert torch.equal(o["spikes"], outs[0]["spikes"])
+        for name in ("grad_x", "grad_alpha", "grad_beta", "grad_kappa", "grad_xi", "grad_zeta"):
+            assert torch.equal(_bits(o["grads"][name]), _bits(outs[0]["grads"][name])), name
+    compare(case, run_gpu(case, gpu_device, dev=d))
+
+
 def test_compartments_checkpoint_interval_is_bit_invariant(gpu_device):
     import torch
 
