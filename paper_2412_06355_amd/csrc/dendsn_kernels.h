@@ -553,12 +553,12 @@ __device__ __forceinline__ void slot_to_lane(const uint32_t (&slot)[kSlotW<W, ST
 // The same pieces moved by the memory unit straight into LDS (buffer loads
 // with the LDS-DMA form): round i writes the 64 lanes' 16-byte pieces to dwords
 // 256 i + 4 lane .. + 3 of `lds`, so the stretch's dword k lands at lds[k] and
-// no register holds it in flight.  A lane past the stretch in the last round
-// fetches the stretch's first piece into the slack past 64 W dwords (an area
-// holds kDmaDw dwords).  The wave reads the area only after its vector memory
-// counter has drained, and refills it only after its reads of it have
-// completed (LDS reads and the DMA's LDS writes are not ordered otherwise).
-template <int W> constexpr int kDmaDw = 256 * kPieces<W>;
+// no register holds it in flight.  Lanes past the stretch in the last round
+// request nothing, so a row's area is exactly its 64 W dwords.  The wave reads
+// the area only after its vector memory counter has drained, and refills it
+// only after its reads of it have completed (LDS reads and the DMA's LDS
+// writes are not ordered otherwise).
+template <int W> constexpr int kDmaDw = 64 * W;
 typedef __attribute__((address_space(3))) void lds_void_t;
 // s_waitcnt lgkmcnt(0), other counters untouched: every LDS access of the wave
 // has completed.
@@ -580,7 +580,7 @@ __device__ __forceinline__ void dma_pieces(rsrc_t r, uint32_t span, uint32_t* ld
 #pragma unroll
   for (int i = 0; i < kPieces<W>; ++i) {
     const uint32_t d = (uint32_t(i) * 64 + lane) * 4;
-    dma_round(r, span + (in_stretch<W>(i, lane) ? d * 4 : 0u), lds + i * 256);
+    if (in_stretch<W>(i, lane)) dma_round(r, span + d * 4, lds + i * 256);
   }
 }
 
@@ -1751,17 +1751,6 @@ __device__ __forceinline__ void stateless_segment_items(const BwdArgs& ba, const
   visit(cur, false, cur);
 }
 
-// The stateful dendrite's wide fp32 lanes (a lane row of more than 16 bytes,
-// e.g. ten compartments), every segment one chunk (K <= KS): pipelined over the
-// lane's (neuron, segment) visits in the Stateless pipeline's order, but the
-// next visit's X rows and checkpointed compartment state travel by LDS DMA
-// (dma_pieces) into the wave's LDS area, where they wait without registers:
-// the stash of a wide stateful neuron leaves none for rows in flight.  The
-// small per-neuron rows (grad_spikes, grad_v_soma, the checkpointed H) ride in
-// registers.  The dendritic adjoint lam and dH cross segment boundaries in
-// reverse time within one neuron and restart at its last segment.  Rows past a
-// short segment's end are not fetched: the recompute runs over whatever the
-// area holds there, and the adjoint pass skips those steps.
 // The registers of a stateful wide visit in flight (its X rows and
 // checkpointed state travel to LDS): grad_spikes, grad_v_soma and H before the
 // segment.
@@ -1810,14 +1799,17 @@ __device__ __forceinline__ void issue_wide_segment(const BwdArgs& ba, const Lane
 // (dma_pieces) into the wave's LDS area, where they wait without registers:
 // the stash of a wide stateful neuron leaves none for rows in flight.  The
 // small per-neuron rows (grad_spikes, grad_v_soma, the checkpointed H) ride in
-// registers.  The dendritic adjoint lam and dH cross segment boundaries in
-// reverse time within one neuron and restart at its last segment.  Rows past a
-// short segment's end are not fetched: the recompute runs over whatever the
-// area holds there, and the adjoint pass skips those steps.
+// registers, and grad_x leaves as whole pieces through the wave's `stage`
+// buffer (store_gx_staged).  The dendritic adjoint lam and dH cross segment
+// boundaries in reverse time within one neuron and restart at its last
+// segment.  Rows past a short segment's end are not fetched: the recompute
+// runs over whatever the area holds there, and the adjoint pass skips those
+// steps.
 template <typename IO, int BL, int L, int V, int KS, bool FAST>
 __device__ __forceinline__ void stateful_segment_items(const BwdArgs& ba, const LaneOff& lo,
                                                        const Branches<BL, kKC<V>>& br, float alpha, int64_t bt0,
-                                                       int nk, Accum<BL, BL * kKC<V>>& acc, uint32_t* area) {
+                                                       int nk, Accum<BL, BL * kKC<V>>& acc, uint32_t* area,
+                                                       uint32_t* stage) {
   constexpr int E = BL * kKC<V>;
   constexpr int W = E;               // fp32 rows: one dword per compartment
   constexpr int RD = kDmaDw<W>;      // LDS dwords per staged row
@@ -1847,7 +1839,7 @@ __device__ __forceinline__ void stateful_segment_items(const BwdArgs& ba, const 
   issue_wide_segment<IO, BL, V, KS, FAST>(ba, lo, ld.n0, ld.nx0, ld.seg, area, cur);
   next(ld);
   BwdLane<IO, E> bl;
-  bl.stage = nullptr;
+  bl.stage = stage;
   bl.dh_next = 0.0f;
   const uint32_t lane = __lane_id();
   for (int i = 0; i < nvis; ++i) {
@@ -1890,7 +1882,7 @@ __device__ __forceinline__ void stateful_segment_items(const BwdArgs& ba, const 
     Stash<BL, KS, V> st;
     recompute_chunk<BL, L, V, KS, FAST>(a, br, alpha, v0, h0, from_ckpt && h0 >= a.vth, xin, st);
     bl.gxbase = static_cast<IO*>(ba.gx) + cp.nx0;
-    reverse_chunk<IO, BL, L, V, KS, true, false>(ba, lo, br, alpha, beta_r, c0, st, gsv, gvv, bl, acc, len);
+    reverse_chunk<IO, BL, L, V, KS, true, true>(ba, lo, br, alpha, beta_r, c0, st, gsv, gvv, bl, acc, len);
     next(cp);
   }
 }
@@ -2090,7 +2082,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
     if constexpr (kWideSF) {
       // one chunk per segment, and not the short-sequence case (T = KS = 4,
       // which has its own pipeline)
-      __shared__ uint32_t area[kThreads / 64][(KS + 1) * kDmaDw<W>];
+      __shared__ uint32_t area[kThreads / 64][(KS + 1) * kDmaDw<W>];   // rows in flight
+      __shared__ uint32_t stage_sf[kThreads / 64][64 * W];              // grad_x leaving
       const uint32_t span = __builtin_amdgcn_readfirstlane(lo.x);
       if (full && a.K <= KS && !(KS == 4 && int(a.T) == KS) && stage_rows<IO>(a, span, bt0)) {
         lo.xw = span;
@@ -2098,9 +2091,11 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(B
 #pragma unroll
         for (int j = 0; j < BL; ++j) all_on = all_on && br.on[j];
         if (__all(all_on) && !ba.gv)
-          stateful_segment_items<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6]);
+          stateful_segment_items<IO, BL, L, V, KS, true>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6],
+                                                          stage_sf[threadIdx.x >> 6]);
         else
-          stateful_segment_items<IO, BL, L, V, KS, false>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6]);
+          stateful_segment_items<IO, BL, L, V, KS, false>(ba, lo, br, alpha, bt0, nk, acc, area[threadIdx.x >> 6],
+                                                           stage_sf[threadIdx.x >> 6]);
         done = true;
       }
     }
