@@ -566,12 +566,13 @@ constexpr int kWaitLds = 0xC07F;
 
 // One round: the wave's 64 pieces at byte offsets `off` (per lane) into the 256
 // dwords at `lds` (a plain function: the LDS-DMA builtin inside a template
-// instantiated by the host compilation pass is rejected there).  Default cache
-// policy: measured on MI355X, non-temporal DMA loads made the stateful P = 10
-// backward 3.5 % faster alone but the kernel launched after it (the forward)
-// 14 % slower, the whole step 0.6 % slower.
+// instantiated by the host compilation pass is rejected there).  Non-temporal,
+// like every whole-line stream here (measured on MI355X, stateful P = 10
+// backward: 375 -> 370 us alone, 388 -> 351 us back to back with the forward;
+// with the default policy the X lines it leaves in the caches only served a
+// forward of the same layer launched right after it, as no training step does).
 __device__ __forceinline__ void dma_round(rsrc_t r, uint32_t off, uint32_t* lds) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, kAuxNT);
 }
 
 template <int W>
