@@ -78,3 +78,57 @@ def test_noalloc_twice_on_a_shrinking_layer(gpu_device):
         ref, out = _both(case, gpu_device)
         _assert_identical(ref, out)
         assert np.isfinite(out["grad_x"].float().cpu().numpy()).all()
+
+
+# A training step (forward, then the allocation-free backward) captured in a
+# HIP graph through torch and replayed: every replay, with eager work and
+# synchronisations between them, matches the eager step bit for bit.
+def test_noalloc_step_under_graph_capture(gpu_device):
+    import torch
+
+    cfg = dendsn.DendSNConfig(T=8, batch=4, C=64, S=300, B=8, ckpt_every=4, beta=0.5, v_th=1.0, psi="mexhat",
+                              sg="sigmoid", sg_scale=4.0)
+    case = make_case(cfg, seed=21, mask_rho=0.6, with_gv=True, name="noalloc/graph")
+    d = to_device(case, gpu_device)
+    f32 = dict(dtype=torch.float32, device=gpu_device)
+    spikes = torch.empty((cfg.T, cfg.N), **f32)
+    ckpt = torch.empty((dendsn.dendsn_ckpt_bytes(cfg) // 4,), **f32)
+    out = dict(grad_x=torch.empty_like(d["x"]), grad_alpha=torch.empty((1,), **f32),
+               grad_beta=torch.empty((1,), **f32), grad_kappa=torch.empty((cfg.C, cfg.B), **f32),
+               grad_xi=torch.empty((cfg.C, cfg.P), **f32), grad_zeta=torch.empty((cfg.C, cfg.B), **f32))
+
+    def step():
+        dendsn.dendsn_forward(cfg, d["x"], d["alpha"], d["beta"], d["kappa"], d["xi"], d["zeta"], d["mask"],
+                              spikes, None, ckpt)
+        dendsn.dendsn_backward_noalloc(cfg, d["x"], d["alpha"], d["beta"], d["kappa"], d["xi"], d["zeta"],
+                                       d["mask"], ckpt, d["gS"], d["gV"], out["grad_x"], out["grad_alpha"],
+                                       out["grad_beta"], out["grad_kappa"], out["grad_xi"], out["grad_zeta"])
+
+    announce(f"graph capture of a noalloc step: {cfg}")
+    step()  # eager (also looks up the scratch array's address before any capture)
+    torch.cuda.synchronize(gpu_device)
+    ref = {k: v.clone() for k, v in out.items()}
+    ref["spikes"] = spikes.clone()
+
+    side = torch.cuda.Stream(device=gpu_device)
+    side.wait_stream(torch.cuda.current_stream(gpu_device))
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream(gpu_device).wait_stream(side)
+    torch.cuda.synchronize(gpu_device)
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize(gpu_device)
+
+    bits = lambda t: t.contiguous().view(torch.uint8)
+    for rep in range(3):
+        for t in list(out.values()) + [spikes]:
+            t.fill_(float("nan"))  # eager work between replays
+        torch.cuda.synchronize(gpu_device)
+        graph.replay()
+        torch.cuda.synchronize(gpu_device)
+        for k, v in out.items():
+            assert torch.equal(bits(v), bits(ref[k])), (rep, k)
+        assert torch.equal(bits(spikes), bits(ref["spikes"])), (rep, "spikes")
