@@ -21,7 +21,7 @@ hipError_t launch_fwd_f32(const Plan& pl, const FwdArgs& fa, int v, hipStream_t 
   const dim3 grid(static_cast<unsigned>(pl.ntiles * pl.G));
 #define DENDSN_CASE(BL_, L_) \
   if (pl.BL == BL_ && pl.L == L_) return launch_fwd_v<BL_, L_>(grid, fa, v, size_t(pl.lds), stream);
-  DENDSN_FAST_F32(DENDSN_CASE)
+  DENDSN_FAST_F32_FWD(DENDSN_CASE)
   DENDSN_GENERIC(DENDSN_CASE)
 #undef DENDSN_CASE
   return hipErrorInvalidValue;

@@ -123,6 +123,8 @@ constexpr int variant_bits(int v) { return (v & 3) | ((v & 4) << 4); }
 // Backward stash capacities: 4 steps for every mapping, and 8 steps too when a
 // lane holds at most 4 branches.
 #define DENDSN_FAST_F32(X) X(4, 1) X(4, 2) X(4, 4) X(4, 8) X(4, 16)
+// The fp32 forward also holds 8 branches per lane over two lanes (16 branches).
+#define DENDSN_FAST_F32_FWD(X) DENDSN_FAST_F32(X) X(8, 2)
 #define DENDSN_FAST_BF16(X) X(4, 1) X(8, 1) X(8, 2) X(8, 4) X(8, 8) X(8, 16)
 // The bf16 backward also holds 4 branches per lane (8 bytes) up to 64 branches.
 #define DENDSN_FAST_BF16_BWD(X) DENDSN_FAST_BF16(X) X(4, 2) X(4, 4) X(4, 8) X(4, 16)

@@ -64,6 +64,11 @@ SHAPES = [
     (13, 2, 6, 1, 8, "bf16", 13),
     (10, 2, 4, 100, 2, "f32", 10),
     (6, 2, 20, 1, 16, "bf16", 3),     # bf16 backward splits a neuron differently from the forward
+    # fp32 16 branches: the forward holds 8 per lane over two lanes (32-byte rows,
+    # staged), the backward 4 over four; conv tiles with four positions per lane
+    (4, 2, 3, 700, 16, "f32", 4),     # forward fast path, a ragged last tile
+    (5, 2, 3, 600, 16, "f32", 3),     # general forward path with checkpoints
+    (8, 2, 2, 1100, 16, "f32", 4),    # padded-free T = 8 with an interior checkpoint
     (4, 2, 9, 40, 32, "bf16", 4),
     (5, 2, 3, 1, 64, "bf16", 2),
     # fully connected, 8 or more lanes per neuron: the backward's two batch ways
