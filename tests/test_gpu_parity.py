@@ -210,6 +210,8 @@ WIDE_STATEFUL = [
     (9, 2, 2, 256, 7, 2, 3),     # 56-byte lane rows (a partial last round of pieces), segments of 3
     (3, 2, 4, 64, 5, 2, 3),      # T < 4: one segment of 3 steps
     (6, 2, 2, 256, 3, 4, 4),     # k = 4, 48-byte rows (whole rounds of pieces only); segments 4, 2
+    (4, 2, 4, 96, 5, 2, 4),      # T = K = 4: every neuron one segment
+    (4, 3, 3, 300, 7, 2, 4),     # T = 4, 56-byte rows, conv tiles with a ragged last tile
 ]
 
 
