@@ -282,16 +282,20 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
     // lane: 464 -> 435 us; B = 8 over two lanes: 934 -> 872 us, 923 with nw = 2);
     // bf16 8-byte rows lost 2-6 % (nw = 4 over two lanes: -1.3 %, not kept).
     // Forward: nw = 4 when a neuron spans several lanes (cifar 411 -> 395 us), 2
-    // for fp32 with one lane per neuron (P = 4 on B = 2: 209 -> 199 us; 4 no
-    // better); one-lane bf16 neurons and channel-major neurons over several
-    // lanes gained nothing and keep 1.
+    // for fp32 with one lane per neuron and 16-byte rows (P = 4 on B = 2: 209 ->
+    // 199 us; 4 no better), 1 for wider one-lane fp32 rows in the
+    // compartments-innermost layout (twice the waves at three per SIMD; ten
+    // compartments, T = 10: 175.8 -> 171.2 us Stateless, 206.8 -> 198.9 us
+    // stateful; the channel-major cifar layer's one-lane forward keeps 2: 417
+    // against 453 us); one-lane bf16 neurons and channel-major neurons over
+    // several lanes gained nothing and keep 1.
     int nw = 1;
     if (bwd) {
       if (c->T == 4 && p.BL * p.KC * esz == 16) nw = L == 1 ? 2 : 4;
     } else if (L >= 2) {
       nw = p.cm ? 1 : 4;
     } else if (esz == 4) {
-      nw = 2;
+      nw = (!p.cm && p.BL * p.KC * esz > 16) ? 1 : 2;
     }
     while (nw > 1 && c->S % (nw * p.pb) != 0) nw /= 2;
     p.nw = nw;
