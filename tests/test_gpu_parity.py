@@ -181,6 +181,7 @@ KC_SHAPES = [
     (4, 2, 3, 300, 5, 2, "f32", 4),      # generic P = 10, conv tiles: a ragged last tile
     (4, 2, 4, 96, 5, 2, "bf16", 4),      # generic bf16 P = 10 (20-byte lane rows), one chunk
     (10, 2, 4, 96, 5, 2, "bf16", 4),     # the same over three checkpoint segments
+    (10, 2, 2, 512, 5, 2, "f32", 4),     # P = 10 over 512-position maps: forward one position per lane
 ]
 
 
@@ -212,6 +213,7 @@ WIDE_STATEFUL = [
     (6, 2, 2, 256, 3, 4, 4),     # k = 4, 48-byte rows (whole rounds of pieces only); segments 4, 2
     (4, 2, 4, 96, 5, 2, 4),      # T = K = 4: every neuron one segment
     (4, 3, 3, 300, 7, 2, 4),     # T = 4, 56-byte rows, conv tiles with a ragged last tile
+    (10, 2, 2, 512, 5, 2, 4),    # 512-position maps: whole tiles, the forward one position per lane
 ]
 
 
