@@ -319,14 +319,17 @@ Plan make_plan(const dendsn_cfg* c, bool bwd) {
   }
   // Batch groups (measured on MI355X): the backward wants ~24K waves in the grid
   // for fp32 rows in the compartments-innermost layout (against ~16K: CIFAR-shaped
-  // -0.5 to -1.1 %, P = 4 on B = 2 -1.5 %, the ResStateless layer -0.6 %; 32K was
-  // 1-3 % slower), ~32K in the channel-major layout (against ~16K: CIFAR-shaped
-  // -1.1 %, P = 4 on B = 2 -0.8 %; ~64K -0.4 % and -2.8 %) and ~16K otherwise
-  // (with 24K: bf16 CIFAR +1.5 %); more groups mean more partial sums to reduce.  The
+  // -0.5 to -1.1 %; ten compartments with 32K: +1-2 %), ~32K where such a row is
+  // one lane's 16 bytes (P = 4 on B = 2 against ~24K: CIFAR-shaped -1.7 %, the
+  // ResStateless layer -0.8 %; ~64K no better) and in the channel-major layout
+  // (against ~16K: CIFAR-shaped -1.1 %, P = 4 on B = 2 -0.8 %; ~64K -0.4 % and
+  // -2.8 %), and ~16K otherwise (with 24K: bf16 CIFAR +1.5 %); more groups mean
+  // more partial sums to reduce.  The
   // forward over conv layers does best with one batch item per lane for fp32
   // (with the XCD eighths below: 1.5-4 % faster than two or four) and eight
   // neurons (batch items x positions) per lane for bf16 (4-5 % faster than four).
-  const int64_t target_waves = p.cm ? 32768 : (esz == 4 ? 24576 : 16384);
+  const bool lane16 = esz == 4 && L == 1 && p.BL * p.KC * esz == 16;
+  const int64_t target_waves = (p.cm || lane16) ? 32768 : (esz == 4 ? 24576 : 16384);
   int64_t G = ceil_div(target_waves, p.ntiles * 4);
   if (!bwd && p.mode == kSpatial) G = esz == 2 ? ceil_div(c->batch * p.nw, 8) : c->batch;
   // fully connected tiles (both directions): four batch items per wave (dbg: the
